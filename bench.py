@@ -1,0 +1,200 @@
+#!/usr/bin/env python3
+"""Benchmark: prefix-shared attention forward + backward on one MI355X.
+
+One step = psattn_fwd + psattn_bwd over the whole tree of one workload (one
+attention layer), inputs resident in HBM, plan built and uploaded once
+outside the timed region.  Prints ONE JSON line (rank 0).
+
+metric: effective (unshared-equivalent) fwd+bwd attention tokens/s = Nu / t_step,
+plus the bf16 MFMA fraction of the dominant kernel and of the whole path.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 matrix
+PEAK_HBM_GBS = 8000.0
+METRIC = "effective fwd+bwd attention tokens/sec (unshared-equiv) + % bf16 MFMA peak"
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_25683_amd", "csrc", "psattn_kernels.hip")
+
+# matmul flops each kernel executes per visible (query, key) pair and query head, per unit of head_dim
+FLOPS_PER_PAIR_PER_D = {"fwd_main": 4, "bwd_kv": 8, "bwd_dq": 6}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c2", help="workload: c1..c5 (c2 is the metric's workload)")
+    ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle sample (0 disables the cpu_baseline leg)")
+    ap.add_argument("--no-profile", action="store_true", help="do not bracket kernels with timing events")
+    return ap.parse_args()
+
+
+def kernel_traffic(kernel, config):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it matches the current kernels."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{config}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if kv.get("kernel_source_sha256") != src_hash:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, seconds):
+    """The fp64 oracle, as it stands, on a bounded sample of the same workload (host cores)."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    t = wl.tree
+    rows = O.sample_rows(t.parent, t.seg_len, t.row_off, t.sample_end)
+    s = 0
+    idx = rows[s]
+    G = wl.hq // wl.hkv
+    heads_done = 0
+    t0 = time.perf_counter()
+    for h in range(wl.hq):
+        q = wl.Q[idx, h].astype(np.float64)
+        k = wl.K[idx, h // G].astype(np.float64)
+        v = wl.V[idx, h // G].astype(np.float64)
+        do = wl.dO[idx, h].astype(np.float64)
+        o, lse = O.causal_fwd(q, k, v, wl.scale)
+        O.causal_bwd(q, k, v, o, lse, do, wl.scale)
+        heads_done += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    el = time.perf_counter() - t0
+    tokens = len(idx) * heads_done / wl.hq      # unshared-equivalent tokens (all Hq heads = 1 token)
+    return {"value": tokens / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"sample 0 ({len(idx)} tokens) x {heads_done} of {wl.hq} query heads, fwd+bwd, fp64 numpy; "
+                      f"{el:.1f} s wall"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the prefix-shared attention path is a single-GPU kernel "
+              "(multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2608_25683_amd import workloads as W
+    from paper_2608_25683_amd import psattn as P
+
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    wl = W.make(a.config)
+    t_gen = time.perf_counter() - t0
+    st = wl.stats()
+    t0 = time.perf_counter()
+    tree = P.Tree.from_workload(wl)
+    t_plan = time.perf_counter() - t0
+    tree.upload(dev)
+    bf16 = wl.dtype == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    Q = torch.from_numpy(wl.Q).to(dev).to(dt)
+    K = torch.from_numpy(wl.K_pool).to(dev).to(dt)
+    V = torch.from_numpy(wl.V_pool).to(dev).to(dt)
+    dO = torch.from_numpy(wl.dO).to(dev).to(dt)
+    ns, hq, hkv, d = tree.num_rows, wl.hq, wl.hkv, wl.d
+    O_ = torch.empty((ns, hq, d), dtype=dt, device=dev)
+    LSE = torch.empty((hq, ns), dtype=torch.float32, device=dev)
+    dQ = torch.empty((ns, hq, d), dtype=torch.float32, device=dev)
+    dK = torch.empty((tree.pool_slots, hkv, d), dtype=torch.float32, device=dev)
+    dV = torch.empty_like(dK)
+    ws_f = tree.workspace(0)
+    ws_b = tree.workspace(1)
+
+    def step():
+        P.psattn_fwd(tree, Q, K, V, O_, LSE, ws_f)
+        P.psattn_bwd(tree, Q, K, V, O_, LSE, dO, dQ, dK, dV, ws_b)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    P.psattn_profile_reset()
+    P.psattn_profile_enable(not a.no_profile)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record()
+    for _ in range(a.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    P.psattn_profile_enable(False)
+    ms_total = ev0.elapsed_time(ev1)
+    ms_step = ms_total / a.steps
+    kern = P.psattn_profile_read() if not a.no_profile else {}
+    P.psattn_profile_reset()
+
+    nu = st["Nu"]
+    value = nu / (ms_step / 1e3)
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    path_tflops = st["flop_alg"] / (ms_step / 1e3) / 1e12
+    roof = None
+    per_kernel = {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in kern.items()}
+    if kern:
+        dom = max(kern, key=lambda k: kern[k][1])
+        n_launch, ms_sum = kern[dom]
+        avg_ms = ms_sum / n_launch
+        if dom in FLOPS_PER_PAIR_PER_D:
+            flops = FLOPS_PER_PAIR_PER_D[dom] * d * hq * st["sum_nvis"]
+            achieved = flops / (avg_ms / 1e3) / 1e12
+            roof = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                    "frac": achieved / peak, "traffic": kernel_traffic(dom, a.config),
+                    "flops_per_launch": flops, "avg_ms": avg_ms}
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{a.config}: {W.CONFIGS[a.config][6]}", "Ns": st["Ns"], "Nu": nu,
+                   "hq": hq, "hkv": hkv, "head_dim": d, "sum_visible_pairs": st["sum_nvis"],
+                   "flop_alg": st["flop_alg"], "parallelism": "single GPU"},
+        "path_mfma": {"achieved": path_tflops, "peak": peak, "unit": "TFLOP/s", "frac": path_tflops / peak,
+                      "flops": "14*d*Hq*sum_visible_pairs"},
+        "roofline": roof,
+        "kernels": per_kernel,
+        "plan_ms": t_plan * 1e3,
+        "wall_s_timed": wall,
+    }
+    if a.cpu_baseline_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(wl, a.cpu_baseline_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

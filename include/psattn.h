@@ -1,0 +1,195 @@
+/*
+ * psattn.h -- prefix-shared causal attention, forward and backward, on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (psRL, arXiv 2608.25683):
+ *   A batch of training samples forms a prefix forest: every node is one
+ *   shared token segment whose K/V is stored once, and every sample is a
+ *   root-to-node path (Sec. 2.3 sampling modes; Sec. 5.2, each tree node is a
+ *   KV block and common prefixes merge).  Attention masking (Sec. 2.5): a
+ *   token at position a of node n attends to every token of n's strict
+ *   ancestors and to tokens 0..a of n, so the shared result equals
+ *   independent causal attention over each sample.  K/V are located through
+ *   per-block metadata {base, size, position, reference count} (Sec. 6,
+ *   "Adaptive KV cache manager" and "Prefix-sharing training runtime"), with
+ *   block sizes that follow the shared spans (Sec. 5.1, adaptive block
+ *   allocation).  The backward pass takes the accumulated adjoint of every
+ *   consumer of a shared token and runs once (Sec. 6, training runtime).
+ *
+ * Layouts (row-major, all device pointers 16-byte aligned):
+ *   Q, O, dO        [Ns][Hq][d]      Ns = sum of segment lengths, rows of node
+ *                                    i at row_off[i] .. row_off[i]+seg_len[i]-1
+ *   dQ              [Ns][Hq][d]      fp32
+ *   K, V            [pool_slots][Hkv][d]   token t of a block at slot base+t
+ *   dK, dV          [pool_slots][Hkv][d]   fp32; slots holding no token are
+ *                                    written 0
+ *   LSE             [Hq][Ns]         fp32, natural log of the softmax
+ *                                    denominator (scale included)
+ *   dtype PSATTN_BF16: Q/K/V/O/dO bf16; LSE/dQ/dK/dV fp32.
+ *   dtype PSATTN_FP32: every tensor fp32.
+ *   Query head h reads key/value head h / (Hq/Hkv).
+ *
+ * Ownership: the caller owns every device buffer (inputs, outputs, the plan
+ * buffer given to psattn_tree_upload, and the workspaces).  The library owns
+ * only the host-side psattn_tree.  psattn_fwd / psattn_bwd allocate nothing,
+ * never synchronise, and enqueue their kernels on the given stream (a
+ * hipStream_t passed as void*, NULL = the null stream); a device fault inside
+ * a kernel surfaces at the caller's next synchronisation.  A tree is
+ * immutable after creation; calls on different streams are safe with
+ * distinct workspaces and outputs.
+ *
+ * Errors: every call returns a psattn_status; on failure nothing is
+ * enqueued, no output of *out is set, and psattn_last_error() (thread-local)
+ * holds a message naming the offending field.  No C++ exception crosses this
+ * interface.
+ */
+#ifndef PSATTN_H
+#define PSATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PSATTN_OK = 0,
+  PSATTN_E_INVALID_ARG = -1,     /* null pointer, bad count or option */
+  PSATTN_E_INVALID_TREE = -2,    /* parent order, empty segment, row layout, sample, refcount */
+  PSATTN_E_BLOCK_RANGE = -3,     /* block outside the pool, or len > capacity */
+  PSATTN_E_BLOCK_OVERLAP = -4,   /* two blocks share a pool slot */
+  PSATTN_E_BLOCK_COVERAGE = -5,  /* blocks do not cover a node's tokens exactly, or pos mismatch */
+  PSATTN_E_UNSUPPORTED = -6,     /* head_dim, dtype or size outside what the kernels handle */
+  PSATTN_E_WORKSPACE = -7,       /* workspace or plan buffer too small */
+  PSATTN_E_ALIGNMENT = -8,       /* device pointer not 16-byte aligned */
+  PSATTN_E_HIP = -9,             /* a HIP runtime call failed (message has the HIP error) */
+  PSATTN_E_NOT_UPLOADED = -10    /* psattn_fwd/bwd called before psattn_tree_upload */
+} psattn_status;
+
+typedef enum { PSATTN_BF16 = 0, PSATTN_FP32 = 1 } psattn_dtype;
+
+/* One page-table entry: the per-block metadata of Sec. 6 (base address,
+ * block size, position of the token segment in the full sequence, reference
+ * count).  A node's blocks are listed in token order. */
+typedef struct {
+  int64_t base;      /* first pool slot of the block */
+  int32_t capacity;  /* slots reserved for the block (its size) */
+  int32_t len;       /* tokens held, 1..capacity, in slots base..base+len-1 */
+  int32_t pos;       /* sequence position of the block's first token (sum of
+                        ancestor lengths + tokens of earlier blocks of the node) */
+  int32_t refcount;  /* 0 = not given; otherwise must equal the number of
+                        samples whose path holds the block (Sec. 5.2) */
+} psattn_block;
+
+typedef struct {
+  int32_t num_nodes;
+  const int32_t* parent;      /* [num_nodes]; parent[i] < i, or -1 for a root (forests allowed) */
+  const int32_t* seg_len;     /* [num_nodes]; >= 1 */
+  const int64_t* row_off;     /* [num_nodes]; the row ranges must tile [0, Ns) exactly */
+  const int32_t* blk_ptr;     /* [num_nodes+1]; node i owns blocks[blk_ptr[i] .. blk_ptr[i+1]) */
+  const psattn_block* blocks;
+  int64_t pool_slots;         /* slots in the K/V pool (< 2^31) */
+  int32_t num_samples;
+  const int32_t* sample_end;  /* [num_samples]; endpoint node of each sample's path */
+  int32_t hq, hkv, head_dim;  /* Hq % Hkv == 0; head_dim 64 or 128 */
+  float softmax_scale;        /* > 0, finite; usually 1/sqrt(head_dim) */
+  psattn_dtype dtype;
+} psattn_tree_desc;
+
+/* Planner knobs.  Zero-initialise for the defaults. */
+typedef struct {
+  int32_t fwd_kv_split;   /* 0 auto; > 0 max keys per forward work item (rounded up to 64); < 0 never split */
+  int32_t bwd_q_chunk;    /* 0 auto; > 0 max query rows per dK/dV work item (rounded up to 32); < 0 never split */
+  int32_t num_cus;        /* compute units to balance for; 0 = 256 */
+  int32_t reserved[5];    /* must be 0 */
+} psattn_plan_opts;
+
+/* Opaque handle: a validated tree, its page-table view and its work plan. */
+typedef struct psattn_tree psattn_tree;
+
+/* Summary of a planned tree (host-side figures). */
+typedef struct {
+  int64_t num_rows;         /* Ns */
+  int64_t unshared_tokens;  /* Nu = sum over samples of path length */
+  int64_t visible_pairs;    /* sum over rows of visible keys (per query head) */
+  int64_t fwd_items, fwd_merges, bkv_items, bkv_reduces, pad_slots;
+  int64_t fwd_partial_rows, bkv_partial_tiles;
+  int64_t plan_bytes;       /* == psattn_tree_device_bytes */
+  int32_t q_tile_rows, kv_tile_keys, bkv_tile_keys, head_chunk;
+} psattn_tree_info;
+
+/* Validate a descriptor, build the page-table view and the work plan (host
+ * only; no GPU call).  Sec. 5.2 (reference counts from the prefix tree),
+ * Sec. 4.2 Eq. "single_sequence" and greedy placement (cost model and
+ * longest-first ordering of work items).  opts may be NULL. */
+psattn_status psattn_tree_create(const psattn_tree_desc* desc, const psattn_plan_opts* opts,
+                                 psattn_tree** out);
+void psattn_tree_destroy(psattn_tree* tree);
+
+/* Bytes of device memory the plan needs (caller allocates, >= 256-byte aligned). */
+psattn_status psattn_tree_device_bytes(const psattn_tree* tree, size_t* bytes);
+
+/* Copy the plan into dev_buf on stream and wait for the copy.  Must precede
+ * psattn_fwd/psattn_bwd; dev_buf must outlive every later call on the tree. */
+psattn_status psattn_tree_upload(psattn_tree* tree, void* dev_buf, size_t bytes, void* stream);
+
+/* Workspace bytes for pass 0 (psattn_fwd) or 1 (psattn_bwd); may be 0. */
+psattn_status psattn_workspace_size(const psattn_tree* tree, int pass, size_t* bytes);
+
+/* Forward (Sec. 2.5 attention masking over the shared layout):
+ *   O[r][h]   = sum_j P_rj V[slot(j)][h/G],  P_r = softmax_j(scale * Q[r][h] . K[slot(j)][h/G])
+ *   LSE[h][r] = log sum_j exp(scale * Q[r][h] . K[slot(j)][h/G])
+ * over the keys j visible to row r.  Long key ranges may be split across
+ * work items and merged by log-sum-exp.  ws may be NULL when its size is 0. */
+psattn_status psattn_fwd(const psattn_tree* tree, const void* Q, const void* K, const void* V,
+                         void* O, float* LSE, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward (Sec. 6: one backward pass over the accumulated adjoints).  dO is
+ * the total adjoint of each shared token.  With P as above,
+ * Delta_r = dO_r . O_r and dS = P * (dO V^T - Delta):
+ *   dQ = scale * dS K;  dK = scale * dS^T Q;  dV = P^T dO
+ * where prefix dK/dV sum over every consuming branch and query head of the
+ * group.  Partial sums are reduced in a fixed order (no floating-point
+ * atomics): results are bitwise reproducible for a given tree and plan. */
+psattn_status psattn_bwd(const psattn_tree* tree, const void* Q, const void* K, const void* V,
+                         const void* O, const float* LSE, const void* dO,
+                         float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes, void* stream);
+
+/* Reference count of every node: the number of samples whose path holds it
+ * (Sec. 5.2).  node_refcount has num_nodes entries. */
+psattn_status psattn_tree_refcounts(const psattn_tree* tree, int32_t* node_refcount);
+
+psattn_status psattn_tree_get_info(const psattn_tree* tree, psattn_tree_info* info);
+
+/* Read-only view of a host plan array, for inspection and tests.  which:
+ *   0 row_pos [Ns]            sequence position of each packed row
+ *   1 q_list                  packed row indices referenced by work items
+ *   2 kv_list                 pool slots referenced by work items
+ *   3 fwd_items [n][8]        q_off nq kv_off nkv kv_pos0 head0 part nfull
+ *   4 fwd_merges [n][4]       q_off nq part0 nparts
+ *   5 bkv_items [n][8]        kv_off nk kv_pos0 q_off nq hk part nmask
+ *   6 bkv_reduces [n][8]      kv_off nk hk part0 nparts 0 0 0
+ *   7 pad_slots [n]           pool slots that hold no token
+ * *data stays valid until psattn_tree_destroy. */
+psattn_status psattn_tree_plan_array(const psattn_tree* tree, int which, const int32_t** data,
+                                     int64_t* count, int32_t* width);
+
+/* Kernel timing for measurement: when enabled, every kernel launch made by
+ * psattn_fwd/psattn_bwd is bracketed by HIP events recorded on its stream.
+ * psattn_profile_read waits for the recorded events and reports, per kernel
+ * name, the launch count and the summed duration in milliseconds since the
+ * last reset.  Not thread-safe; meant for single-threaded benchmarking. */
+psattn_status psattn_profile_enable(int enable);
+psattn_status psattn_profile_reset(void);
+psattn_status psattn_profile_read(int32_t max_entries, int32_t* num_entries, const char** names,
+                                  int64_t* launches, double* total_ms);
+
+const char* psattn_status_string(psattn_status status);
+const char* psattn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PSATTN_H */

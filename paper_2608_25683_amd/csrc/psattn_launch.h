@@ -1,0 +1,51 @@
+// Kernel launchers (defined in psattn_kernels.hip, called by the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "psattn_plan.h"
+
+namespace psattn {
+
+struct FwdArgs {
+  PlanView plan;
+  Shape s;
+  int32_t n_items, n_merge;
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* O;
+  float* LSE;
+  float* part_o;    // [partial rows][Hq][d]
+  float* part_lse;  // [partial rows][Hq]
+};
+
+struct BwdArgs {
+  PlanView plan;
+  Shape s;
+  int32_t n_fwd, n_merge, n_bkv, n_reduce, n_pad;
+  const void* Q;
+  const void* K;
+  const void* V;
+  const void* O;
+  const float* LSE;
+  const void* dO;
+  float* dQ;
+  float* dK;
+  float* dV;
+  float* delta;    // [Hq][Ns]
+  float* part_dq;  // [partial rows][Hq][d]
+  float* part_dk;  // [partial tiles][BKV_TILE][d]; each tile belongs to one kv head
+  float* part_dv;
+};
+
+// Each launcher enqueues one kernel on stream and returns the launch status.
+hipError_t launch_fwd_main(const FwdArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_fwd_merge(const FwdArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_bwd_reduce_kv(const BwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_reduce_dq(const BwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_zero_pad(const BwdArgs& a, hipStream_t st);
+
+}  // namespace psattn

@@ -1,0 +1,332 @@
+"""Python binding of libpsattn (ctypes).  Argument marshalling only.
+
+Every step of the forward and backward pass runs in the HIP kernels of
+libpsattn.so; torch provides device memory and the current stream.  There
+is no fallback: if the library is missing, or a tensor is not on a GPU,
+the call raises.
+
+Names follow the C ABI in include/psattn.h:
+    Tree(...)                       psattn_tree_create / _upload / _destroy
+    psattn_fwd(tree, Q, K, V)       -> (O, LSE)
+    psattn_bwd(tree, Q, K, V, O, LSE, dO) -> (dQ, dK, dV)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpsattn.so")
+
+PSATTN_BF16 = 0
+PSATTN_FP32 = 1
+
+STATUS = {
+    0: "PSATTN_OK", -1: "PSATTN_E_INVALID_ARG", -2: "PSATTN_E_INVALID_TREE", -3: "PSATTN_E_BLOCK_RANGE",
+    -4: "PSATTN_E_BLOCK_OVERLAP", -5: "PSATTN_E_BLOCK_COVERAGE", -6: "PSATTN_E_UNSUPPORTED",
+    -7: "PSATTN_E_WORKSPACE", -8: "PSATTN_E_ALIGNMENT", -9: "PSATTN_E_HIP", -10: "PSATTN_E_NOT_UPLOADED",
+}
+
+EXPORTED = [
+    "psattn_tree_create", "psattn_tree_destroy", "psattn_tree_device_bytes", "psattn_tree_upload",
+    "psattn_workspace_size", "psattn_fwd", "psattn_bwd", "psattn_tree_refcounts", "psattn_tree_get_info",
+    "psattn_tree_plan_array", "psattn_profile_enable", "psattn_profile_reset", "psattn_profile_read",
+    "psattn_status_string", "psattn_last_error",
+]
+
+PLAN_ARRAYS = {"row_pos": 0, "q_list": 1, "kv_list": 2, "fwd_items": 3, "fwd_merges": 4, "bkv_items": 5,
+               "bkv_reduces": 6, "pad_slots": 7}
+
+
+class PsattnError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+class Block(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_int64), ("capacity", ctypes.c_int32), ("len", ctypes.c_int32),
+                ("pos", ctypes.c_int32), ("refcount", ctypes.c_int32)]
+
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+
+
+class TreeDesc(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_int32), ("parent", _i32p), ("seg_len", _i32p), ("row_off", _i64p),
+                ("blk_ptr", _i32p), ("blocks", ctypes.POINTER(Block)), ("pool_slots", ctypes.c_int64),
+                ("num_samples", ctypes.c_int32), ("sample_end", _i32p), ("hq", ctypes.c_int32),
+                ("hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("dtype", ctypes.c_int32)]
+
+
+class PlanOpts(ctypes.Structure):
+    _fields_ = [("fwd_kv_split", ctypes.c_int32), ("bwd_q_chunk", ctypes.c_int32), ("num_cus", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 5)]
+
+
+class TreeInfo(ctypes.Structure):
+    _fields_ = [("num_rows", ctypes.c_int64), ("unshared_tokens", ctypes.c_int64), ("visible_pairs", ctypes.c_int64),
+                ("fwd_items", ctypes.c_int64), ("fwd_merges", ctypes.c_int64), ("bkv_items", ctypes.c_int64),
+                ("bkv_reduces", ctypes.c_int64), ("pad_slots", ctypes.c_int64), ("fwd_partial_rows", ctypes.c_int64),
+                ("bkv_partial_tiles", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("q_tile_rows", ctypes.c_int32),
+                ("kv_tile_keys", ctypes.c_int32), ("bkv_tile_keys", ctypes.c_int32), ("head_chunk", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libpsattn.so (built in-tree by __graft_entry__.build()); raise if it is missing."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz = ctypes.c_void_p, ctypes.c_size_t
+        L.psattn_tree_create.argtypes = [ctypes.POINTER(TreeDesc), ctypes.POINTER(PlanOpts), ctypes.POINTER(vp)]
+        L.psattn_tree_destroy.argtypes = [vp]
+        L.psattn_tree_destroy.restype = None
+        L.psattn_tree_device_bytes.argtypes = [vp, ctypes.POINTER(sz)]
+        L.psattn_tree_upload.argtypes = [vp, vp, sz, vp]
+        L.psattn_workspace_size.argtypes = [vp, ctypes.c_int, ctypes.POINTER(sz)]
+        L.psattn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.psattn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.psattn_tree_refcounts.argtypes = [vp, _i32p]
+        L.psattn_tree_get_info.argtypes = [vp, ctypes.POINTER(TreeInfo)]
+        L.psattn_tree_plan_array.argtypes = [vp, ctypes.c_int, ctypes.POINTER(_i32p), _i64p, _i32p]
+        L.psattn_profile_enable.argtypes = [ctypes.c_int]
+        L.psattn_profile_reset.argtypes = []
+        L.psattn_profile_read.argtypes = [ctypes.c_int32, _i32p, ctypes.POINTER(ctypes.c_char_p), _i64p,
+                                          ctypes.POINTER(ctypes.c_double)]
+        L.psattn_status_string.argtypes = [ctypes.c_int]
+        L.psattn_status_string.restype = ctypes.c_char_p
+        L.psattn_last_error.argtypes = []
+        L.psattn_last_error.restype = ctypes.c_char_p
+        for name in EXPORTED:
+            if name not in ("psattn_tree_destroy", "psattn_status_string", "psattn_last_error"):
+                getattr(L, name).restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise PsattnError(status, lib().psattn_last_error().decode())
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+class Tree:
+    """A validated prefix tree + page table + work plan (psattn_tree_create).
+
+    Arrays follow psattn_tree_desc.  ``opts`` is a dict of psattn_plan_opts
+    fields.  Call :meth:`upload` (or pass ``device``) before psattn_fwd/bwd.
+    """
+
+    def __init__(self, parent, seg_len, row_off, blk_ptr, blk_base, blk_cap, blk_len, blk_pos, pool_slots,
+                 sample_end, hq, hkv, head_dim, softmax_scale, dtype="bf16", blk_refcount=None, opts=None,
+                 device=None):
+        L = lib()
+        self._handle = None
+        self.parent = np.ascontiguousarray(parent, dtype=np.int32)
+        self.seg_len = np.ascontiguousarray(seg_len, dtype=np.int32)
+        self.row_off = np.ascontiguousarray(row_off, dtype=np.int64)
+        self.blk_ptr = np.ascontiguousarray(blk_ptr, dtype=np.int32)
+        self.sample_end = np.ascontiguousarray(sample_end, dtype=np.int32)
+        nb = len(blk_base)
+        blocks = (Block * max(nb, 1))()
+        rc = np.zeros(nb, dtype=np.int64) if blk_refcount is None else np.asarray(blk_refcount)
+        for i in range(nb):
+            blocks[i] = Block(int(blk_base[i]), int(blk_cap[i]), int(blk_len[i]), int(blk_pos[i]), int(rc[i]))
+        self.dtype = dtype
+        self.hq, self.hkv, self.head_dim = int(hq), int(hkv), int(head_dim)
+        self.scale = float(softmax_scale)
+        self.pool_slots = int(pool_slots)
+        desc = TreeDesc(len(self.parent), _ptr(self.parent, ctypes.c_int32), _ptr(self.seg_len, ctypes.c_int32),
+                        _ptr(self.row_off, ctypes.c_int64), _ptr(self.blk_ptr, ctypes.c_int32), blocks,
+                        int(pool_slots), len(self.sample_end), _ptr(self.sample_end, ctypes.c_int32), self.hq,
+                        self.hkv, self.head_dim, self.scale, PSATTN_BF16 if dtype == "bf16" else PSATTN_FP32)
+        o = PlanOpts()
+        for k, v in (opts or {}).items():
+            if k == "reserved":
+                for i, x in enumerate(v):
+                    o.reserved[i] = int(x)
+            else:
+                setattr(o, k, int(v))
+        h = ctypes.c_void_p()
+        _check(L.psattn_tree_create(ctypes.byref(desc), ctypes.byref(o), ctypes.byref(h)))
+        self._handle = h
+        info = TreeInfo()
+        _check(L.psattn_tree_get_info(h, ctypes.byref(info)))
+        self.info = info.as_dict()
+        self.num_rows = int(self.info["num_rows"])
+        self._plan_buf = None
+        self._ws = {}
+        if device is not None:
+            self.upload(device)
+
+    @classmethod
+    def from_workload(cls, wl, opts=None, device=None, **kw):
+        t = wl.tree
+        return cls(t.parent, t.seg_len, t.row_off, t.blk_ptr, t.blk_base, t.blk_cap, t.blk_len, t.blk_pos,
+                   t.pool_slots, t.sample_end, wl.hq, wl.hkv, wl.d, wl.scale, dtype=wl.dtype, opts=opts,
+                   device=device, **kw)
+
+    @property
+    def handle(self):
+        return self._handle
+
+    def __del__(self):
+        if getattr(self, "_handle", None) is not None and _LIB is not None:
+            _LIB.psattn_tree_destroy(self._handle)
+            self._handle = None
+
+    def device_bytes(self) -> int:
+        n = ctypes.c_size_t()
+        _check(lib().psattn_tree_device_bytes(self._handle, ctypes.byref(n)))
+        return n.value
+
+    def workspace_size(self, pass_: int) -> int:
+        n = ctypes.c_size_t()
+        _check(lib().psattn_workspace_size(self._handle, pass_, ctypes.byref(n)))
+        return n.value
+
+    def upload(self, device="cuda"):
+        import torch
+        nbytes = self.device_bytes()
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        stream = torch.cuda.current_stream(buf.device).cuda_stream
+        _check(lib().psattn_tree_upload(self._handle, ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(stream)))
+        self._plan_buf = buf
+        self.device = buf.device
+        return self
+
+    def workspace(self, pass_: int):
+        """A cached workspace tensor for pass 0 (fwd) or 1 (bwd), allocated through torch."""
+        import torch
+        n = self.workspace_size(pass_)
+        ws = self._ws.get(pass_)
+        if ws is None or ws.numel() < n:
+            ws = torch.empty(max(n, 256), dtype=torch.uint8, device=self.device)
+            self._ws[pass_] = ws
+        return ws
+
+    def refcounts(self) -> np.ndarray:
+        out = np.zeros(len(self.parent), dtype=np.int32)
+        _check(lib().psattn_tree_refcounts(self._handle, _ptr(out, ctypes.c_int32)))
+        return out
+
+    def plan_array(self, name: str) -> np.ndarray:
+        data = _i32p()
+        count = ctypes.c_int64()
+        width = ctypes.c_int32()
+        _check(lib().psattn_tree_plan_array(self._handle, PLAN_ARRAYS[name], ctypes.byref(data), ctypes.byref(count),
+                                            ctypes.byref(width)))
+        n = count.value * width.value
+        if n == 0:
+            return np.zeros((0, width.value) if width.value > 1 else (0,), dtype=np.int32)
+        arr = np.ctypeslib.as_array(data, shape=(n,)).copy()
+        return arr.reshape(count.value, width.value) if width.value > 1 else arr
+
+
+def _torch_dtype(tree):
+    import torch
+    return torch.bfloat16 if tree.dtype == "bf16" else torch.float32
+
+
+def _need(t, shape, dtype, name):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise RuntimeError(f"{name} must be on a GPU (the HIP path has no CPU fallback)")
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+def _vp(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def psattn_fwd(tree: Tree, Q, K, V, O=None, LSE=None, ws=None):
+    """Forward pass on the current stream; returns (O [Ns,Hq,d], LSE [Hq,Ns] fp32)."""
+    import torch
+    if tree._plan_buf is None:
+        raise RuntimeError("tree not uploaded (call Tree.upload)")
+    dt = _torch_dtype(tree)
+    ns, hq, hkv, d = tree.num_rows, tree.hq, tree.hkv, tree.head_dim
+    _need(Q, (ns, hq, d), dt, "Q")
+    _need(K, (tree.pool_slots, hkv, d), dt, "K")
+    _need(V, (tree.pool_slots, hkv, d), dt, "V")
+    if O is None:
+        O = torch.empty((ns, hq, d), dtype=dt, device=Q.device)
+    if LSE is None:
+        LSE = torch.empty((hq, ns), dtype=torch.float32, device=Q.device)
+    _need(O, (ns, hq, d), dt, "O")
+    _need(LSE, (hq, ns), torch.float32, "LSE")
+    if ws is None:
+        ws = tree.workspace(0)
+    stream = torch.cuda.current_stream(Q.device).cuda_stream
+    _check(lib().psattn_fwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(ws), ws.numel(),
+                            ctypes.c_void_p(stream)))
+    return O, LSE
+
+
+def psattn_bwd(tree: Tree, Q, K, V, O, LSE, dO, dQ=None, dK=None, dV=None, ws=None):
+    """Backward pass on the current stream; returns (dQ, dK, dV), all fp32."""
+    import torch
+    if tree._plan_buf is None:
+        raise RuntimeError("tree not uploaded (call Tree.upload)")
+    dt = _torch_dtype(tree)
+    ns, hq, hkv, d, ps = tree.num_rows, tree.hq, tree.hkv, tree.head_dim, tree.pool_slots
+    _need(Q, (ns, hq, d), dt, "Q")
+    _need(K, (ps, hkv, d), dt, "K")
+    _need(V, (ps, hkv, d), dt, "V")
+    _need(O, (ns, hq, d), dt, "O")
+    _need(LSE, (hq, ns), torch.float32, "LSE")
+    _need(dO, (ns, hq, d), dt, "dO")
+    f32 = torch.float32
+    if dQ is None:
+        dQ = torch.empty((ns, hq, d), dtype=f32, device=Q.device)
+    if dK is None:
+        dK = torch.empty((ps, hkv, d), dtype=f32, device=Q.device)
+    if dV is None:
+        dV = torch.empty((ps, hkv, d), dtype=f32, device=Q.device)
+    _need(dQ, (ns, hq, d), f32, "dQ")
+    _need(dK, (ps, hkv, d), f32, "dK")
+    _need(dV, (ps, hkv, d), f32, "dV")
+    if ws is None:
+        ws = tree.workspace(1)
+    stream = torch.cuda.current_stream(Q.device).cuda_stream
+    _check(lib().psattn_bwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(dO), _vp(dQ), _vp(dK),
+                            _vp(dV), _vp(ws), ws.numel(), ctypes.c_void_p(stream)))
+    return dQ, dK, dV
+
+
+def psattn_profile_enable(on: bool = True) -> None:
+    _check(lib().psattn_profile_enable(1 if on else 0))
+
+
+def psattn_profile_reset() -> None:
+    _check(lib().psattn_profile_reset())
+
+
+def psattn_profile_read() -> dict:
+    """{kernel name: (launches, total ms)} since the last reset (waits for the recorded events)."""
+    n = ctypes.c_int32()
+    cap = 16
+    names = (ctypes.c_char_p * cap)()
+    launches = (ctypes.c_int64 * cap)()
+    ms = (ctypes.c_double * cap)()
+    _check(lib().psattn_profile_read(cap, ctypes.byref(n), names, launches, ms))
+    return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(min(n.value, cap))}

@@ -1,0 +1,287 @@
+"""Host-side tests of libpsattn through its C ABI (no GPU needed).
+
+* the shared library loads and exports every function include/psattn.h declares;
+* descriptor validation returns the documented status for each kind of bad input;
+* the planner's work items cover every visible (query, key) pair exactly once,
+  in the forward/dQ items and in the dK/dV items, and never leave an invisible
+  pair unmasked (brute force over random forests);
+* reference counts (Sec. 5.2) and the adaptive-block example (Sec. 5.1).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_25683_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+P = pytest.importorskip("paper_2608_25683_amd.psattn")
+
+if not os.path.exists(P.LIB_PATH):
+    pytest.skip("libpsattn.so not built", allow_module_level=True)
+
+
+def test_library_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "psattn.h")).read()
+    declared = set(re.findall(r"\b(psattn_[a-z_]+)\s*\(", hdr))
+    assert declared == set(P.EXPORTED), declared ^ set(P.EXPORTED)
+    lib = ctypes.CDLL(P.LIB_PATH)
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    L = P.lib()
+    for code, name in P.STATUS.items():
+        assert L.psattn_status_string(code).decode() == name
+
+
+# --------------------------------------------------------------------------- descriptor validation
+
+def _desc_arrays(wl):
+    t = wl.tree
+    return dict(parent=t.parent.copy(), seg_len=t.seg_len.copy(), row_off=t.row_off.copy(), blk_ptr=t.blk_ptr.copy(),
+                blk_base=t.blk_base.copy(), blk_cap=t.blk_cap.copy(), blk_len=t.blk_len.copy(),
+                blk_pos=t.blk_pos.copy(), pool_slots=t.pool_slots, sample_end=t.sample_end.copy(), hq=wl.hq,
+                hkv=wl.hkv, head_dim=wl.d, softmax_scale=wl.scale, dtype=wl.dtype)
+
+
+def _make(**kw):
+    return P.Tree(**kw)
+
+
+@pytest.fixture
+def base():
+    # root(10) -> a(5), root -> b(7); a -> c(3); samples c, b
+    wl = W.custom([-1, 0, 0, 1], [10, 5, 7, 3], [3, 2], hq=4, hkv=2, d=128, tensors=False,
+                  block_policy=lambda L: W.blocks_fixed(L, 4), shuffle_pool=True, seed=5)
+    return _desc_arrays(wl)
+
+
+def test_valid_descriptor_is_accepted(base):
+    t = _make(**base)
+    assert t.num_rows == 25
+    assert t.info["unshared_tokens"] == (10 + 5 + 3) + (10 + 7)
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda d: d["parent"].__setitem__(1, 1), "PSATTN_E_INVALID_TREE"),        # parent not before child
+    (lambda d: d["parent"].__setitem__(2, 7), "PSATTN_E_INVALID_TREE"),        # out of range
+    (lambda d: d["seg_len"].__setitem__(3, 0), "PSATTN_E_INVALID_TREE"),       # empty segment
+    (lambda d: d["row_off"].__setitem__(2, 14), "PSATTN_E_INVALID_TREE"),      # rows overlap / gap
+    (lambda d: d["sample_end"].__setitem__(0, 9), "PSATTN_E_INVALID_TREE"),    # bad sample endpoint
+    (lambda d: d.__setitem__("sample_end", np.array([2], np.int32)), "PSATTN_E_INVALID_TREE"),  # unreachable nodes
+    (lambda d: d["blk_len"].__setitem__(0, 5), "PSATTN_E_BLOCK_RANGE"),        # len > capacity
+    (lambda d: d["blk_base"].__setitem__(0, 10 ** 6), "PSATTN_E_BLOCK_RANGE"),  # outside the pool
+    (lambda d: d["blk_base"].__setitem__(1, d["blk_base"][0]), "PSATTN_E_BLOCK_OVERLAP"),
+    (lambda d: d["blk_pos"].__setitem__(1, 3), "PSATTN_E_BLOCK_COVERAGE"),     # pos mismatch
+    (lambda d: d["blk_len"].__setitem__(2, 1), "PSATTN_E_BLOCK_COVERAGE"),     # blocks do not cover the node
+    (lambda d: d.__setitem__("hq", 5), "PSATTN_E_UNSUPPORTED"),               # hq % hkv != 0
+    (lambda d: d.__setitem__("head_dim", 96), "PSATTN_E_UNSUPPORTED"),
+    (lambda d: d.__setitem__("softmax_scale", float("nan")), "PSATTN_E_INVALID_ARG"),
+    (lambda d: d.__setitem__("pool_slots", 0), "PSATTN_E_UNSUPPORTED"),
+])
+def test_invalid_descriptors(base, mutate, status):
+    mutate(base)
+    with pytest.raises(P.PsattnError) as e:
+        _make(**base)
+    assert e.value.name == status, str(e.value)
+
+
+def test_wrong_refcount_is_rejected(base):
+    rc = np.zeros(len(base["blk_base"]), dtype=np.int64)
+    rc[0] = 99
+    with pytest.raises(P.PsattnError) as e:
+        _make(blk_refcount=rc, **base)
+    assert e.value.name == "PSATTN_E_INVALID_TREE"
+
+
+def test_opts_reserved_must_be_zero(base):
+    with pytest.raises(P.PsattnError) as e:
+        _make(opts={"reserved": [1, 0, 0, 0, 0]}, **base)
+    assert e.value.name == "PSATTN_E_INVALID_ARG"
+
+
+def test_calls_before_upload_fail(base):
+    t = _make(**base)
+    L = P.lib()
+    st = L.psattn_fwd(t.handle, *(ctypes.c_void_p(64),) * 5, None, 0, None)
+    assert P.STATUS[st] == "PSATTN_E_NOT_UPLOADED"
+    st = L.psattn_workspace_size(t.handle, 2, ctypes.byref(ctypes.c_size_t()))
+    assert P.STATUS[st] == "PSATTN_E_INVALID_ARG"
+    assert P.STATUS[L.psattn_tree_create(None, None, ctypes.byref(ctypes.c_void_p()))] == "PSATTN_E_INVALID_ARG"
+
+
+# --------------------------------------------------------------------------- paper structure examples
+
+def test_refcounts_of_the_dbc_example():
+    # Sec. 5.2 / Fig. "Generation_Prefix_Tree": samples a, b, c, d; root read by all four,
+    # a second block read by a, b, c, a third block read by a only.
+    # Tree: root -> X -> {Ya, Yb, Yc}; root -> Yd.  Samples end at Ya, Yb, Yc, Yd.
+    wl = W.custom([-1, 0, 1, 1, 1, 0], [6, 4, 3, 2, 5, 4], [2, 3, 4, 5], tensors=False, seed=1)
+    t = P.Tree.from_workload(wl)
+    assert list(t.refcounts()) == [4, 3, 1, 1, 1, 1]
+
+
+def test_adaptive_block_example():
+    # Sec. 5.1 / Fig. "Block_Management": two 32-token sequences share tokens 0..27 and diverge at 28..31.
+    # Adaptive blocks: one 28-token shared block plus two 4-token blocks, no padding.
+    aba = W.custom([-1, 0, 0], [28, 4, 4], [1, 2], tensors=False, block_policy=W.blocks_exact)
+    t = P.Tree.from_workload(aba)
+    assert list(aba.tree.blk_len) == [28, 4, 4] and aba.tree.pool_slots == 36
+    assert t.info["pad_slots"] == 0 and t.info["unshared_tokens"] == 64
+    # fixed 32-token blocks on the same tree: 3 blocks of 32 slots, 60 of them padding
+    fixed = W.custom([-1, 0, 0], [28, 4, 4], [1, 2], tensors=False, block_policy=lambda L: W.blocks_fixed(L, 32))
+    t2 = P.Tree.from_workload(fixed)
+    assert fixed.tree.pool_slots == 96 and t2.info["pad_slots"] == 60
+
+
+def test_named_config_plan_sizes():
+    for name in ("c1", "c2", "c3", "c4", "c5"):
+        tree, _ = W.make_tree(name)
+        seed, hq, hkv, d, dtype, *_ = W.CONFIGS[name]
+        t = P.Tree(tree.parent, tree.seg_len, tree.row_off, tree.blk_ptr, tree.blk_base, tree.blk_cap,
+                   tree.blk_len, tree.blk_pos, tree.pool_slots, tree.sample_end, hq, hkv, d, d ** -0.5, dtype)
+        st = W.tree_stats(tree, hq, d)
+        assert t.info["visible_pairs"] == st["sum_nvis"]
+        assert t.info["unshared_tokens"] == st["Nu"]
+        assert t.info["pad_slots"] == tree.pool_slots - st["Ns"]
+
+
+# --------------------------------------------------------------------------- planner coverage (brute force)
+
+def _visible_pairs(tree):
+    """Set of (row, key_row) pairs of the tree mask."""
+    off = tree.node_offsets()
+    pairs = set()
+    for n in range(tree.num_nodes):
+        prow = np.concatenate([np.arange(tree.row_off[m], tree.row_off[m] + tree.seg_len[m]) for m in tree.path(n)])
+        for a in range(int(tree.seg_len[n])):
+            r = int(tree.row_off[n]) + a
+            for k in prow[: int(off[n]) + a + 1]:
+                pairs.add((r, int(k)))
+    return pairs
+
+
+def _check_plan(wl, t):
+    tree = wl.tree
+    G = wl.hq // wl.hkv
+    slots = tree.row_slots()
+    slot_to_row = {int(s): r for r, s in enumerate(slots)}
+    row_pos = t.plan_array("row_pos")
+    q_list = t.plan_array("q_list")
+    kv_list = t.plan_array("kv_list")
+    fwd = t.plan_array("fwd_items")
+    merges = t.plan_array("fwd_merges")
+    bkv = t.plan_array("bkv_items")
+    reds = t.plan_array("bkv_reduces")
+    pad = t.plan_array("pad_slots")
+    hc = t.info["head_chunk"]
+    bmq = t.info["q_tile_rows"]
+    visible = _visible_pairs(tree)
+    off = tree.node_offsets()
+    for n in range(tree.num_nodes):
+        for a in range(int(tree.seg_len[n])):
+            assert row_pos[tree.row_off[n] + a] == off[n] + a
+
+    # forward / dQ items: every visible pair once per query head
+    cover = {}
+    for q_off, nq, kv_off, nkv, kv_pos0, head0, part, nfull in fwd:
+        rows = q_list[q_off:q_off + nq]
+        assert 1 <= nq <= bmq and head0 % hc == 0
+        keys = [slot_to_row[int(s)] for s in kv_list[kv_off:kv_off + nkv]]
+        minq = min(row_pos[r] for r in rows)
+        for t_ in range(nfull):   # tiles declared mask-free must be fully visible and full
+            assert (t_ + 1) * 64 <= nkv and kv_pos0 + (t_ + 1) * 64 - 1 <= minq
+        for r in rows:
+            for j, k in enumerate(keys):
+                if kv_pos0 + j <= row_pos[r]:
+                    assert (r, k) in visible, ("fwd item attends an invisible key", r, k)
+                    for h in range(head0, head0 + hc):
+                        cover[(h, r, k)] = cover.get((h, r, k), 0) + 1
+    assert all(v == 1 for v in cover.values())
+    assert len(cover) == len(visible) * wl.hq
+    # split pieces belong to a merge entry with the same rows
+    parts = {int(p) for p in fwd[:, 6] if p >= 0}
+    want = set()
+    for q_off, nq, part0, nparts in merges:
+        for j in range(nparts):
+            want.add(int(part0 + j * bmq))
+    assert parts == want
+
+    # dK/dV items: every visible pair once per query head (G heads per kv head)
+    cover = {}
+    for kv_off, nk, kv_pos0, q_off, nq, hk, part, nmask in bkv:
+        keys = [slot_to_row[int(s)] for s in kv_list[kv_off:kv_off + nk]]
+        rows = q_list[q_off:q_off + nq]
+        for i, r in enumerate(rows):
+            if i >= nmask:
+                assert row_pos[r] >= kv_pos0 + nk - 1, "row past nmask sees only part of the tile"
+            for j, k in enumerate(keys):
+                vis = (r, k) in visible
+                if row_pos[r] >= kv_pos0 + j:
+                    # the mask test passes only for pairs of the tree mask
+                    assert vis, ("dK/dV item would use an invisible pair", r, k)
+                    cover[(hk, r, k)] = cover.get((hk, r, k), 0) + 1
+                else:
+                    assert not vis
+    assert all(v == 1 for v in cover.values())
+    assert len(cover) == len(visible) * wl.hkv
+    parts = sorted(int(p) for p in bkv[:, 6] if p >= 0)
+    want = sorted(int(r[3] + j) for r in reds for j in range(r[4]))
+    assert parts == want and len(set(parts)) == len(parts)
+    # pad slots = pool slots holding no token
+    assert set(pad.tolist()) == set(range(tree.pool_slots)) - set(slots.tolist())
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_covers_tree_mask_exactly_once(seed):
+    wl = W.random_forest(100 + seed, max_nodes=9, max_seg=150, hq=4 * (1 + seed % 2), hkv=2, tensors=False,
+                         shuffle_rows=(seed % 3 == 0))
+    opts = {}
+    if seed % 2 == 0:
+        opts = {"fwd_kv_split": 64 * (1 + seed % 3), "bwd_q_chunk": 32 * (1 + seed % 4)}
+    t = P.Tree.from_workload(wl, opts=opts)
+    _check_plan(wl, t)
+
+
+def test_forced_splits_produce_partials():
+    wl = W.custom([-1, 0, 1, 1], [300, 90, 40, 77], [2, 3], hq=8, hkv=2, tensors=False)
+    t = P.Tree.from_workload(wl, opts={"fwd_kv_split": 64, "bwd_q_chunk": 32})
+    assert t.info["fwd_merges"] > 0 and t.info["bkv_reduces"] > 0
+    _check_plan(wl, t)
+    t = P.Tree.from_workload(wl, opts={"fwd_kv_split": -1, "bwd_q_chunk": -1})
+    assert t.info["fwd_merges"] == 0 and t.info["bkv_reduces"] == 0
+    _check_plan(wl, t)
+
+
+@pytest.mark.parametrize("hq,hkv", [(4, 4), (6, 2), (10, 2), (16, 1), (12, 4)])
+def test_plan_head_chunks(hq, hkv):
+    wl = W.random_forest(7, max_nodes=6, max_seg=70, hq=hq, hkv=hkv, tensors=False)
+    t = P.Tree.from_workload(wl)
+    G = hq // hkv
+    hc = t.info["head_chunk"]
+    assert G % hc == 0 and hc <= 8
+    _check_plan(wl, t)
+
+
+def test_plan_is_deterministic():
+    wl = W.random_forest(3, max_nodes=12, max_seg=200, tensors=False)
+    a = P.Tree.from_workload(wl, opts={"fwd_kv_split": 128, "bwd_q_chunk": 64})
+    b = P.Tree.from_workload(wl, opts={"fwd_kv_split": 128, "bwd_q_chunk": 64})
+    for name in P.PLAN_ARRAYS:
+        assert np.array_equal(a.plan_array(name), b.plan_array(name)), name
+
+
+def test_items_are_longest_first():
+    # Eq. "single_sequence" cost (rows x keys) and greedy longest-first order
+    wl = W.make("c4", tensors=False)
+    t = P.Tree.from_workload(wl)
+    fwd = t.plan_array("fwd_items")
+    cost = fwd[:, 1].astype(np.int64) * fwd[:, 3]
+    assert np.all(np.diff(cost) <= 0)
+    bkv = t.plan_array("bkv_items")
+    cost = bkv[:, 1].astype(np.int64) * bkv[:, 4]
+    assert np.all(np.diff(cost) <= 0)

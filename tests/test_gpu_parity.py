@@ -1,0 +1,117 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Tolerances per output tensor (O, LSE, dQ, dK, dV): bf16 inputs with fp32
+accumulation max-abs 2e-2 and relative L2 5e-3; fp32 mode 1e-5 / 1e-5.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2608_25683_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+import parity_helpers as H  # noqa: E402
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# --------------------------------------------------------------------------- small trees, every output element
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_forest_bf16(seed):
+    wl = W.random_forest(200 + seed, max_nodes=8, max_seg=90, hq=8, hkv=2, d=128, dtype="bf16",
+                         shuffle_rows=(seed % 2 == 1))
+    _say(f"random forest bf16 seed={seed} rows={wl.tree.num_rows}")
+    H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_random_forest_forced_splits(seed):
+    wl = W.random_forest(300 + seed, max_nodes=7, max_seg=160, hq=4, hkv=1, d=128, dtype="bf16")
+    _say(f"random forest splits seed={seed} rows={wl.tree.num_rows}")
+    H.check_full(wl, H.run_gpu(wl, opts={"fwd_kv_split": 64, "bwd_q_chunk": 32}), H.run_oracle(wl))
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(5, 1, 128), (8, 8, 64), (2, 1, 64), (12, 2, 128), (16, 2, 64), (3, 1, 128)])
+def test_head_layouts(hq, hkv, d):
+    wl = W.random_forest(400 + hq, max_nodes=5, max_seg=70, hq=hq, hkv=hkv, d=d, dtype="bf16")
+    _say(f"head layout hq={hq} hkv={hkv} d={d}")
+    H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_random_forest_fp32(d):
+    wl = W.random_forest(500 + d, max_nodes=6, max_seg=80, hq=4, hkv=2, d=d, dtype="fp32", sigma=1.0)
+    _say(f"random forest fp32 d={d}")
+    H.check_full(wl, H.run_gpu(wl, opts={"fwd_kv_split": 64, "bwd_q_chunk": 64}), H.run_oracle(wl))
+
+
+def test_c1_full_fp32():
+    wl = W.make("c1")
+    _say("c1 full")
+    res = H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+    _say(f"c1 {res}")
+
+
+# scaled-down versions of the bf16 workloads: several tiles per node and ragged tails
+SMALL = {
+    "c2s": dict(parent=[-1] + [0] * 5, seg=[300] + [150] * 5, samples=list(range(1, 6)), hq=8, hkv=2,
+                policy=lambda L: W.blocks_fixed(L, 64)),
+    "c3s": dict(parent=[-1, 0, 1, -1, 3, 4], seg=[70, 130, 95, 110, 33, 200], samples=list(range(6)), hq=8, hkv=2,
+                policy=W.blocks_greedy),
+    "c4s": dict(parent=[-1, 0, 0, 1, 1, 2, 2], seg=[256, 40, 131, 77, 64, 9, 100], samples=[3, 4, 5, 6], hq=8,
+                hkv=2, policy=lambda L: W.blocks_fixed(L, 32)),
+    "c5s": dict(parent=[-1, 0, 0, -1, 3, 4, 4], seg=[27, 190, 61, 333, 16, 45, 129], samples=list(range(7)), hq=10,
+                hkv=2, policy=W.blocks_exact),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_scaled_down_workloads(name):
+    c = SMALL[name]
+    wl = W.custom(c["parent"], c["seg"], c["samples"], hq=c["hq"], hkv=c["hkv"], d=128, dtype="bf16", seed=7,
+                  block_policy=c["policy"])
+    _say(f"scaled-down {name} rows={wl.tree.num_rows}")
+    H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+
+
+# --------------------------------------------------------------------------- robustness and determinism
+
+def test_bitwise_repeatable():
+    wl = W.random_forest(600, max_nodes=8, max_seg=120, hq=8, hkv=2, dtype="bf16")
+    a, b = H.run_gpu(wl, opts={"fwd_kv_split": 128, "bwd_q_chunk": 64}, reps=2)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_pool_order_and_padding_do_not_change_results():
+    base = dict(parent=[-1, 0, 0, 1], seg_len=[150, 70, 45, 90], samples=[3, 2], hq=8, hkv=2, d=128, dtype="bf16", seed=3)
+    w1 = W.custom(**base, block_policy=lambda L: W.blocks_fixed(L, 64), shuffle_pool=False)
+    w2 = W.custom(**base, block_policy=lambda L: W.blocks_fixed(L, 64), shuffle_pool=True)
+    w3 = W.custom(**base, block_policy=lambda L: W.blocks_fixed(L, 16), shuffle_pool=True)
+    r1, r2, r3 = H.run_gpu(w1), H.run_gpu(w2), H.run_gpu(w3)
+    for i in range(3):   # O, LSE, dQ: row layout is the same
+        assert np.array_equal(r1[i], r2[i]) and np.array_equal(r1[i], r3[i])
+    for i in (3, 4):     # dK, dV: compare token by token
+        for w, r in ((w2, r2), (w3, r3)):
+            assert np.array_equal(r1[i][w1.tree.row_slots()], r[i][w.tree.row_slots()])
+
+
+# --------------------------------------------------------------------------- full-size workloads (sampled)
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_full_size_sampled(name):
+    _say(f"{name}: generating")
+    wl = W.make(name)
+    _say(f"{name}: running GPU")
+    gpu = H.run_gpu(wl)
+    _say(f"{name}: checking sampled outputs")
+    res = H.check_sampled(wl, gpu, kv_heads=(0, wl.hkv - 1))
+    _say(f"{name}: sampled {res}")
+    H.check_identities(wl, gpu)
