@@ -22,7 +22,8 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 matrix
 PEAK_HBM_GBS = 8000.0
 METRIC = "effective fwd+bwd attention tokens/sec (unshared-equiv) + % bf16 MFMA peak"
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_25683_amd", "csrc", "psattn_kernels.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_25683_amd", "csrc", f) for f in
+               ("psattn_device.h", "psattn_fwd.hip", "psattn_bwd.hip")]
 
 # matmul flops each kernel executes per visible (query, key) pair and query head, per unit of head_dim
 FLOPS_PER_PAIR_PER_D = {"fwd_main": 4, "bwd_kv": 8, "bwd_dq": 6}
@@ -50,7 +51,10 @@ def kernel_traffic(kernel, config):
         if ":" in line:
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    src_hash = h.hexdigest()
     if kv.get("kernel_source_sha256") != src_hash:
         return None
     try:

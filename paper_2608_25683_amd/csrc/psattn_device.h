@@ -1,0 +1,103 @@
+// Device-side helpers shared by the HIP kernels (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "psattn_launch.h"
+
+namespace psattn {
+namespace dev {
+
+typedef uint16_t bf16_t;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+
+#define PSATTN_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_inff();
+constexpr int IDX_BLK = 256;   // slot / row indices staged in LDS per block
+
+__device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ bf16x8 as_bf(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ bf16x8 as_bf(const u32x2& lo, const u32x2& hi) {
+  return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+}
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
+__device__ __forceinline__ u32x2 ld8(const void* p) { return *(const u32x2*)p; }
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+}
+__device__ __forceinline__ float bf2f(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+// 8 consecutive accumulator values -> one bf16x8 MFMA operand
+__device__ __forceinline__ bf16x8 pack8(const f32x16& x, int base) {
+  u32x4 w;
+  w[0] = pack2(x[base + 0], x[base + 1]);
+  w[1] = pack2(x[base + 2], x[base + 3]);
+  w[2] = pack2(x[base + 4], x[base + 5]);
+  w[3] = pack2(x[base + 6], x[base + 7]);
+  return as_bf(w);
+}
+
+// Max / sum over the lane pair (l, l ^ 32) with one v_permlane32_swap: whichever half the
+// instruction exchanges, the two results hold this lane's value and its partner's.
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ---- LDS tiles of rows of D bf16 (D*2 bytes per row), no padding.  The 16-byte chunk c of row
+// r lives at chunk position c ^ swz(r), so that 16 consecutive rows read at one column, and
+// 4 consecutive rows x 4 consecutive chunks read by the transposing loads, hit distinct banks.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (r >> 1) & 7;
+}
+template <int D>
+__device__ __forceinline__ int tile_off(int r, int c) {
+  return r * (D * 2) + ((c ^ swz<D>(r)) << 4);
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane i writes lds_base + 16 i.
+// Issued through inline assembly so that the compiler does not wait for the copy before every
+// later LDS read (it cannot tell which LDS bytes the copy writes); the kernels wait explicitly
+// (wait_vmem + barrier) before reading a stage.  lds_base must be wave-uniform.
+__device__ __forceinline__ void copy16_to_lds(const void* g, void* lds_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)PSATTN_LDS(void, lds_base));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+// 4 bytes per lane: lane i writes lds_base + 4 i (inactive lanes write nothing).
+__device__ __forceinline__ void copy4_to_lds(const void* g, void* lds_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)PSATTN_LDS(void, lds_base));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+// Wait until at most N vector-memory loads of this wave are in flight (gfx9 s_waitcnt encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).  The intrinsic keeps
+// the compiler's own load scoreboard in step, so it inserts no further waits for older loads.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Transposing LDS read: within each 16-lane group, lanes 4r..4r+3 point at 4 consecutive bf16 of
+// row r (r = 0..3) and lane i of the group receives column i of those 4 rows.
+__device__ __forceinline__ u32x2 lds_tr(const void* p) {
+  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(PSATTN_LDS(s16x4, p));
+  return __builtin_bit_cast(u32x2, v);
+}
+
+}  // namespace dev
+}  // namespace psattn

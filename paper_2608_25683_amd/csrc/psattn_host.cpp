@@ -230,7 +230,8 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   s.hc = 1;
   for (int c = 8; c >= 1; --c)
     if (s.g % c == 0) { s.hc = c; break; }
-  s.rw = s.hc >= 4 ? 1 : (s.hc == 3 ? 2 : 4 / s.hc);
+  // 32-row subtiles per head: a forward/dQ workgroup holds up to 8 wavefronts (hc x rw)
+  s.rw = (8 % s.hc == 0) ? 8 / s.hc : (s.hc <= 4 ? 2 : 1);
   s.nw = s.hc * s.rw;
   s.bmq = Q_SUB * s.rw;
   s.scale = t->scale;
