@@ -21,68 +21,68 @@ namespace {
 
 using namespace dev;
 
+// 8 wavefronts: wave w owns keys 32*(w%4) .. +31 of the tile and, within each pipeline stage of
+// 32 rows x 2 query heads, the head w/4; the two waves of a key group add their dK/dV partial
+// sums in a fixed order at the end.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_kv_bf16_kernel(BwdArgs a) {
+__global__ __launch_bounds__(512) void bwd_kv_bf16_kernel(BwdArgs a) {
   constexpr int RB = D * 2;
   constexpr int CPR = D / 8;
   constexpr int RPI = 64 / CPR;
-  constexpr int QB = Q_SUB * RB;              // bytes per Q or dO subtile
+  constexpr int QB = Q_SUB * RB;              // bytes per Q or dO subtile of one head
   constexpr int NI = Q_SUB / RPI;             // copy instructions per subtile and tensor
-  constexpr int IPW = NI / 4;                 // per wave
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int SPB = IDX_BLK / Q_SUB;        // subtiles per staged row block
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2][2][QB];   // [stage][Q | dO]
-  __shared__ __attribute__((aligned(16))) float s_stat[2][2][Q_SUB];  // [stage][LSE | Delta][row]
+  constexpr int HPS = 2;                      // query heads per pipeline stage
+  constexpr int KVB = BKV_TILE * RB;          // bytes of the K (or V) tile
+  constexpr int STB = 2 * HPS * 2 * QB;       // bytes of both stages
+  static_assert(2 * KVB + STB >= 4 * 32 * D * 4 * 2, "pair reduction buffer");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * KVB + STB];   // K | V | stages[2][HPS][Q|dO]
+  __shared__ __attribute__((aligned(16))) float s_stat[2][HPS][2][Q_SUB];  // [stage][head][LSE*log2e | Delta]
   __shared__ int s_row[2][IDX_BLK];
   __shared__ int s_qpos[2][IDX_BLK];
   __shared__ int s_slot[BKV_TILE];
+  uint8_t* const s_k = smem;
+  uint8_t* const s_v = smem + KVB;
+  uint8_t* const s_st = smem + 2 * KVB;
+  auto stage_q = [&](int st, int j) { return s_st + ((st * HPS + j) * 2 + 0) * QB; };
+  auto stage_do = [&](int st, int j) { return s_st + ((st * HPS + j) * 2 + 1) * QB; };
 
   const BkvItem it = a.plan.bkv[blockIdx.x];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
+  const int kg = wave & 3, hp = wave >> 2;    // key group, head within a stage
   const int hk = it.hk, G = a.s.g, hq = a.s.hq, ns = a.s.ns;
   const int nq = it.nq;
   const int* ql = a.plan.q_list + it.q_off;
   const size_t kv_stride = (size_t)a.s.hkv * D;
+  const int ngrp = (G + HPS - 1) / HPS;       // stages per 32-row subtile
+  const int crow = lane / CPR, cpc = lane % CPR;
 
   if (tid < BKV_TILE) s_slot[tid] = a.plan.kv_list[it.kv_off + min(tid, it.nk - 1)];
-  {
+  if (tid < IDX_BLK) {
     const int r = ql[min(tid, nq - 1)];
     s_row[0][tid] = r;
     s_qpos[0][tid] = tid < nq ? a.plan.row_pos[r] : -1;
   }
   int pre_row = 0, pre_qpos = -1;
-  if (nq > IDX_BLK) {
+  if (tid < IDX_BLK && nq > IDX_BLK) {
     pre_row = ql[min(IDX_BLK + tid, nq - 1)];
     pre_qpos = IDX_BLK + tid < nq ? a.plan.row_pos[pre_row] : -1;
   }
+  __syncthreads();
+  // K and V rows of the tile into LDS (row-major, swizzled): B operands of S = Q K^T, dP = dO V^T
+#pragma unroll
+  for (int i = 0; i < BKV_TILE / RPI / 8; ++i) {
+    const int k = wave + 8 * i;
+    const int r = k * RPI + crow;
+    const size_t go = (size_t)s_slot[r] * kv_stride + (size_t)hk * D + ((cpc ^ swz<D>(r)) << 3);
+    copy16_to_lds((const bf16_t*)a.K + go, s_k + k * 1024);
+    copy16_to_lds((const bf16_t*)a.V + go, s_v + k * 1024);
+  }
 
-  const int kidx = 32 * wave + l32;
+  const int kidx = 32 * kg + l32;
   const int kpos = it.kv_pos0 + kidx;
-  bf16x8 kreg[KS], vreg[KS];
-  {
-    const int slot = a.plan.kv_list[it.kv_off + min(kidx, it.nk - 1)];
-    const bf16_t* kp = (const bf16_t*)a.K + (size_t)slot * kv_stride + (size_t)hk * D + 8 * hh;
-    const bf16_t* vp = (const bf16_t*)a.V + (size_t)slot * kv_stride + (size_t)hk * D + 8 * hh;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      kreg[s] = as_bf(ld16(kp + 16 * s));
-      vreg[s] = as_bf(ld16(vp + 16 * s));
-    }
-  }
-  int koff[KS];
-#pragma unroll
-  for (int s = 0; s < KS; ++s) koff[s] = tile_off<D>(l32, 2 * s + hh);
-  int voff[2][DB];
-  {
-    const int r4 = (lane & 15) >> 2, j = lane & 3, dsub = 16 * ((lane >> 4) & 1);
-#pragma unroll
-    for (int rd = 0; rd < 2; ++rd)
-#pragma unroll
-      for (int nb = 0; nb < DB; ++nb)
-        voff[rd][nb] = tile_off<D>(8 * rd + 4 * hh + r4, (32 * nb + dsub + 4 * j) >> 3) + 8 * (j & 1);
-  }
-
   f32x16 dk[DB], dv[DB];
 #pragma unroll
   for (int nb = 0; nb < DB; ++nb) {
@@ -91,35 +91,44 @@ __global__ __launch_bounds__(256) void bwd_kv_bf16_kernel(BwdArgs a) {
   }
 
   const int nsub = (nq + Q_SUB - 1) / Q_SUB;
-  const int nsteps = nsub * G;
-  const int crow = lane / CPR, cpc = lane % CPR;
+  const int nsteps = nsub * ngrp;
   auto issue = [&](int step) {
-    const int st = step & 1, sub = step / G, head = hk * G + step % G;
+    const int st = step & 1, sub = step / ngrp, h0 = (step % ngrp) * HPS;
+    const int nh = min(HPS, G - h0);
     const int* rows = &s_row[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
+    // 2 heads x 2 tensors x NI copy instructions over 8 waves
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int k = wave + 4 * i;
-      const int r = k * RPI + crow;
-      const size_t go = ((size_t)rows[r] * hq + head) * D + ((cpc ^ swz<D>(r)) << 3);
-      copy16_to_lds((const bf16_t*)a.Q + go, &smem[st][0][k * 1024]);
-      copy16_to_lds((const bf16_t*)a.dO + go, &smem[st][1][k * 1024]);
+    for (int i = 0; i < (HPS * 2 * NI + 7) / 8; ++i) {
+      const int k = wave + 8 * i;              // (head, tensor, instruction)
+      const int jh = k / (2 * NI), tens = (k / NI) & 1, ins = k % NI;
+      if (k < HPS * 2 * NI && jh < nh) {
+        const int r = ins * RPI + crow;
+        const size_t go = ((size_t)rows[r] * hq + hk * G + h0 + jh) * D + ((cpc ^ swz<D>(r)) << 3);
+        copy16_to_lds((const bf16_t*)(tens ? a.dO : a.Q) + go, (tens ? stage_do(st, jh) : stage_q(st, jh)) + ins * 1024);
+      }
     }
-    if (lane < 16) {
-      const int r = 16 * (wave & 1) + lane;
-      const float* src = (wave >> 1) ? a.delta : a.LSE;
-      copy4_to_lds(src + (size_t)head * ns + rows[r], &s_stat[st][wave >> 1][16 * (wave & 1)]);
+    if (wave < nh) {   // wave j brings LSE*log2e (lanes 0-31) and Delta (lanes 32-63) of head h0 + j
+      const float* src = hh ? a.delta : a.lse2;
+      copy4_to_lds(src + (size_t)(hk * G + h0 + wave) * ns + rows[l32], &s_stat[st][wave][0][0]);
     }
   };
 
   const float c = a.s.scale * kLog2e;
-  wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
+  const int arow = l32 * RB, asw = swz<D>(l32);
+  const int krow = (32 * kg + l32) * RB;      // this lane's key row in the K / V tiles (same swizzle)
+  const int r4 = (lane & 15) >> 2, jq = lane & 3, dsub = 16 * ((lane >> 4) & 1);
+  const int tcol = (dsub + 4 * jq) >> 3, tbyte = 8 * (jq & 1);
+  const int trow0 = (4 * hh + r4) * RB, tsw0 = swz<D>(4 * hh + r4);
+  const int trow1 = (8 + 4 * hh + r4) * RB, tsw1 = swz<D>(8 + 4 * hh + r4);
+
+  wait_vmem<0>();
   __syncthreads();
   issue(0);
   for (int step = 0; step < nsteps; ++step) {
     const int sn = step + 1;
-    const bool new_blk = sn < nsteps && sn % G == 0 && (sn / G) % SPB == 0;
-    if (new_blk) {
-      const int blk = (sn / G) / SPB;
+    const bool new_blk = sn < nsteps && sn % ngrp == 0 && (sn / ngrp) % SPB == 0;
+    if (new_blk && tid < IDX_BLK) {
+      const int blk = (sn / ngrp) / SPB;
       s_row[blk & 1][tid] = pre_row;
       s_qpos[blk & 1][tid] = pre_qpos;
     }
@@ -127,8 +136,8 @@ __global__ __launch_bounds__(256) void bwd_kv_bf16_kernel(BwdArgs a) {
     __syncthreads();
     if (sn < nsteps) {
       issue(sn);
-      if (new_blk) {
-        const int nxt = ((sn / G) / SPB + 1) * IDX_BLK + tid;
+      if (new_blk && tid < IDX_BLK) {
+        const int nxt = ((sn / ngrp) / SPB + 1) * IDX_BLK + tid;
         if (nxt - tid < nq) {
           pre_row = ql[min(nxt, nq - 1)];
           pre_qpos = nxt < nq ? a.plan.row_pos[pre_row] : -1;
@@ -136,47 +145,80 @@ __global__ __launch_bounds__(256) void bwd_kv_bf16_kernel(BwdArgs a) {
       }
     }
 
-    const int st = step & 1, sub = step / G;
-    const uint8_t* Qt = &smem[st][0][0];
-    const uint8_t* dOt = &smem[st][1][0];
+    const int st = step & 1, sub = step / ngrp;
+    const int nh = min(HPS, G - (step % ngrp) * HPS);
+    if (hp >= nh) continue;                    // wave-uniform: this stage has no head for this wave
+    const uint8_t* Qt = stage_q(st, hp);
+    const uint8_t* dOt = stage_do(st, hp);
+    // S = Q K^T and dP = dO V^T (lane <-> key, element v <-> row 8*(v/4) + 4*hh + v%4)
     f32x16 S = f32x16{}, dP = f32x16{};
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      S = mfma(as_bf(ld16(Qt + koff[s])), kreg[s], S);
-      dP = mfma(as_bf(ld16(dOt + koff[s])), vreg[s], dP);
+      const int ch = ((2 * s + hh) ^ asw) << 4;
+      S = mfma(as_bf(ld16(Qt + arow + ch)), as_bf(ld16(s_k + krow + ch)), S);
+      dP = mfma(as_bf(ld16(dOt + arow + ch)), as_bf(ld16(s_v + krow + ch)), dP);
     }
-    // accumulator layout: lane <-> key (column l32), element v <-> row 8*(v/4) + 4*hh + v%4
-    const bool need_mask = (Q_SUB * sub < it.nmask) || (Q_SUB * sub + Q_SUB > nq);
-    const int* qp = &s_qpos[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
-      const f32x4 L = *(const f32x4*)&s_stat[st][0][8 * g4 + 4 * hh];
-      const f32x4 Dl = *(const f32x4*)&s_stat[st][1][8 * g4 + 4 * hh];
+      const f32x4 L2 = *(const f32x4*)&s_stat[st][hp][0][8 * g4 + 4 * hh];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int v = 4 * g4 + e;
-        float p = fast_exp2(fmaf(S[v], c, -L[e] * kLog2e));
-        if (need_mask && kpos > qp[8 * g4 + 4 * hh + e]) p = 0.f;
-        S[v] = p;
-        dP[v] = p * (dP[v] - Dl[e]);
+      for (int e = 0; e < 4; ++e) S[4 * g4 + e] = fast_exp2(fmaf(S[4 * g4 + e], c, -L2[e]));
+    }
+    const int r0 = Q_SUB * sub;
+    if (r0 + Q_SUB > nq || (r0 < it.mask_hi && r0 + Q_SUB > it.mask_lo)) {   // wave-uniform
+      const int* qp = &s_qpos[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int4 q4 = *(const int4*)&qp[8 * g4 + 4 * hh];
+        S[4 * g4 + 0] = kpos > q4.x ? 0.f : S[4 * g4 + 0];
+        S[4 * g4 + 1] = kpos > q4.y ? 0.f : S[4 * g4 + 1];
+        S[4 * g4 + 2] = kpos > q4.z ? 0.f : S[4 * g4 + 2];
+        S[4 * g4 + 3] = kpos > q4.w ? 0.f : S[4 * g4 + 3];
       }
+    }
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const f32x4 Dl = *(const f32x4*)&s_stat[st][hp][1][8 * g4 + 4 * hh];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dP[4 * g4 + e] = S[4 * g4 + e] * (dP[4 * g4 + e] - Dl[e]);
     }
     const bf16x8 pa0 = pack8(S, 0), pa1 = pack8(S, 8);
     const bf16x8 sa0 = pack8(dP, 0), sa1 = pack8(dP, 8);
 #pragma unroll
     for (int nb = 0; nb < DB; ++nb) {
-      dv[nb] = mfma(pa0, as_bf(lds_tr(dOt + voff[0][nb]), lds_tr(dOt + voff[1][nb])), dv[nb]);
-      dv[nb] = mfma(pa1, as_bf(lds_tr(dOt + 16 * RB + voff[0][nb]), lds_tr(dOt + 16 * RB + voff[1][nb])), dv[nb]);
-      dk[nb] = mfma(sa0, as_bf(lds_tr(Qt + voff[0][nb]), lds_tr(Qt + voff[1][nb])), dk[nb]);
-      dk[nb] = mfma(sa1, as_bf(lds_tr(Qt + 16 * RB + voff[0][nb]), lds_tr(Qt + 16 * RB + voff[1][nb])), dk[nb]);
+      // B operands dO^T and Q^T by transposing reads: rows 16t + 8rd + 4hh + r4, column 32nb + l32
+      const int o0 = trow0 + (((4 * nb + tcol) ^ tsw0) << 4) + tbyte;
+      const int o1 = trow1 + (((4 * nb + tcol) ^ tsw1) << 4) + tbyte;
+      dv[nb] = mfma(pa0, as_bf(lds_tr(dOt + o0), lds_tr(dOt + o1)), dv[nb]);
+      dv[nb] = mfma(pa1, as_bf(lds_tr(dOt + 16 * RB + o0), lds_tr(dOt + 16 * RB + o1)), dv[nb]);
+      dk[nb] = mfma(sa0, as_bf(lds_tr(Qt + o0), lds_tr(Qt + o1)), dk[nb]);
+      dk[nb] = mfma(sa1, as_bf(lds_tr(Qt + 16 * RB + o0), lds_tr(Qt + 16 * RB + o1)), dk[nb]);
     }
   }
 
-  // accumulator layout: lane <-> head_dim column 32*nb + l32, element v <-> key of this wave
+  // fixed-order pair sum: the head-1 wave of each key group parks its partial sums in LDS
+  __syncthreads();
+  float* park = (float*)smem + (size_t)kg * (2 * DB * 16 * 64);
+  if (hp == 1) {
+#pragma unroll
+    for (int nb = 0; nb < DB; ++nb) {
+      *(f32x16*)(park + ((0 * DB + nb) * 64 + lane) * 16) = dk[nb];
+      *(f32x16*)(park + ((1 * DB + nb) * 64 + lane) * 16) = dv[nb];
+    }
+  }
+  __syncthreads();
+  if (hp == 1) return;
+#pragma unroll
+  for (int nb = 0; nb < DB; ++nb) {
+    dk[nb] += *(const f32x16*)(park + ((0 * DB + nb) * 64 + lane) * 16);
+    dv[nb] += *(const f32x16*)(park + ((1 * DB + nb) * 64 + lane) * 16);
+  }
+
+  // accumulator layout: lane <-> head_dim column 32*nb + l32, element v <-> key of this group
   const float scale = a.s.scale;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    const int key = 32 * wave + 8 * (v >> 2) + 4 * hh + (v & 3);
+    const int key = 32 * kg + 8 * (v >> 2) + 4 * hh + (v & 3);
     if (key >= it.nk) continue;
     float* kdst;
     float* vdst;
@@ -220,7 +262,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_bf16_kernel(BwdArgs a) {
   const bool row_ok = ridx < it.nq;
   const int row = a.plan.q_list[it.q_off + (row_ok ? ridx : it.nq - 1)];
   const int qpos = a.plan.row_pos[row];
-  const float lse2 = a.LSE[(size_t)head * a.s.ns + row] * kLog2e;
+  const float lse2 = a.lse2[(size_t)head * a.s.ns + row];
   const float del = a.delta[(size_t)head * a.s.ns + row];
   const int nkv = it.nkv;
   const int* kvl = a.plan.kv_list + it.kv_off;
@@ -498,7 +540,8 @@ __global__ __launch_bounds__(512) void bwd_dq_f32_kernel(BwdArgs a) {
 }
 
 // ============================================================================================
-// Delta = rowsum(dO * O) per (row, head); D/8 lanes per (row, head), 8 elements each
+// Delta = rowsum(dO * O) per (row, head), and LSE * log2(e) for the exp2-based kernels;
+// D/8 lanes per (row, head), 8 elements each
 template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   const int D = a.s.d, hq = a.s.hq;
@@ -527,7 +570,9 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   for (int w = lanes / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
   if (ok && sub == 0) {
     const int row = rh / hq, h = rh % hq;
-    a.delta[(size_t)h * a.s.ns + row] = acc;
+    const size_t o = (size_t)h * a.s.ns + row;
+    a.delta[o] = acc;
+    a.lse2[o] = a.LSE[o] * kLog2e;
   }
 }
 
@@ -600,8 +645,8 @@ hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st) {
 hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_bkv), block(256);
   if (bf16) {
-    if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_kernel<128>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((bwd_kv_bf16_kernel<64>), grid, block, 0, st, a);
+    if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_kernel<128>), grid, dim3(512), 0, st, a);
+    else hipLaunchKernelGGL((bwd_kv_bf16_kernel<64>), grid, dim3(512), 0, st, a);
   } else {
     if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_f32_kernel<128>), grid, block, 0, st, a);
     else hipLaunchKernelGGL((bwd_kv_f32_kernel<64>), grid, block, 0, st, a);

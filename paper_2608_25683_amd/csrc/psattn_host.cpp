@@ -334,11 +334,12 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   }
 
   // ---------------- dK/dV tasks: key tile x consumer-row chunk ----------------
-  // consumer list of node m: its own rows, then every row of every descendant
-  std::vector<int64_t> cons_off(N), cons_len(N);
+  // consumer list of node m: every row of every descendant (node order), then m's own rows from
+  // its last position down to 0; the tile starting at key b0 uses the list up to own position b0
+  std::vector<int64_t> cons_off(N), cons_len(N), desc_len(N);
   for (int m = 0; m < N; ++m) {
     cons_off[m] = (int64_t)t->q_list.size();
-    std::vector<int> stack{m};
+    std::vector<int> stack(t->children[m].begin(), t->children[m].end());
     std::vector<int> sub;
     while (!stack.empty()) {
       int x = stack.back();
@@ -346,9 +347,11 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       sub.push_back(x);
       for (int c : t->children[x]) stack.push_back(c);
     }
-    std::sort(sub.begin(), sub.end());  // m first (smallest id in its subtree), then node order
+    std::sort(sub.begin(), sub.end());
     for (int x : sub)
       for (int a = 0; a < t->seg_len[x]; ++a) t->q_list.push_back((int32_t)(t->row_off[x] + a));
+    desc_len[m] = (int64_t)t->q_list.size() - cons_off[m];
+    for (int a = t->seg_len[m] - 1; a >= 0; --a) t->q_list.push_back((int32_t)(t->row_off[m] + a));
     cons_len[m] = (int64_t)t->q_list.size() - cons_off[m];
     if (t->q_list.size() > (size_t)INT32_MAX) return fail(PSATTN_E_UNSUPPORTED, "row lists exceed 2^31 entries");
   }
@@ -367,7 +370,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     int64_t per_cu = total_b * t->hkv / std::max(1, 2 * num_cus);
     chunk_rows = std::max<int64_t>(2048, per_cu / BKV_TILE / Q_SUB * Q_SUB);
   }
-  struct BTask { int32_t kv_off, nk, kv_pos0, q_off, nq, nmask, part_base, nparts, chunk; double cost; };
+  struct BTask { int32_t kv_off, nk, kv_pos0, q_off, nq, mask_lo, mask_hi, part_base, nparts, chunk; double cost; };
   std::vector<BTask> btasks;
   std::vector<ReduceEntry> reduces;
   int64_t part_tiles = 0;
@@ -375,6 +378,8 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     for (int b0 = 0; b0 < t->seg_len[m]; b0 += BKV_TILE) {
       int nk = std::min(BKV_TILE, t->seg_len[m] - b0);
       int64_t nq_total = cons_len[m] - b0;
+      // own rows at positions b0 .. b0+nk-2 see only part of the tile: the last nk-1 list entries
+      const int64_t mlo = nq_total - (nk - 1), mhi = nq_total;
       int nparts = chunk_rows == INT64_MAX ? 1 : (int)((nq_total + chunk_rows - 1) / chunk_rows);
       int32_t kv_off = (int32_t)(kvoff[m] + t->off[m] + b0);
       int32_t kv_pos0 = (int32_t)(t->off[m] + b0);
@@ -391,11 +396,10 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
         b.kv_off = kv_off;
         b.nk = nk;
         b.kv_pos0 = kv_pos0;
-        b.q_off = (int32_t)(cons_off[m] + b0 + c0);
+        b.q_off = (int32_t)(cons_off[m] + c0);
         b.nq = (int32_t)(c1 - c0);
-        // own-node rows at positions < b0 + nk - 1 may see only part of the tile
-        int64_t nm = (int64_t)(nk - 1) - c0;
-        b.nmask = (int32_t)std::max<int64_t>(0, std::min<int64_t>(nm, b.nq));
+        b.mask_lo = (int32_t)std::min<int64_t>(std::max<int64_t>(mlo - c0, 0), b.nq);
+        b.mask_hi = (int32_t)std::min<int64_t>(std::max<int64_t>(mhi - c0, 0), b.nq);
         b.part_base = part_base;
         b.nparts = nparts;
         b.chunk = j;
@@ -415,7 +419,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       const BTask& b = btasks[i];
       for (int hk = 0; hk < t->hkv; ++hk) {
         int32_t part = b.nparts > 1 ? b.part_base + hk * b.nparts + b.chunk : -1;
-        t->bkv.push_back({b.kv_off, b.nk, b.kv_pos0, b.q_off, b.nq, hk, part, b.nmask});
+        t->bkv.push_back({b.kv_off, b.nk, b.kv_pos0, b.q_off, b.nq, hk, part, b.mask_lo, b.mask_hi, 0});
       }
     }
   }
@@ -490,11 +494,13 @@ FwdWs fwd_ws(const psattn_tree* t) {
   w.total = t->fwd_part_rows ? cur : 0;
   return w;
 }
-struct BwdWs { size_t o_delta, o_part_dq, o_part_dk, o_part_dv, total; };
+struct BwdWs { size_t o_delta, o_lse2, o_part_dq, o_part_dk, o_part_dv, total; };
 BwdWs bwd_ws(const psattn_tree* t) {
   BwdWs w;
   size_t cur = 0;
   w.o_delta = cur;
+  cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
+  w.o_lse2 = cur;
   cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
   w.o_part_dq = cur;
   cur = align_up(cur + (size_t)t->fwd_part_rows * t->hq * t->d * 4);
@@ -681,6 +687,7 @@ psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, con
   a.dV = dV;
   uint8_t* wb = (uint8_t*)ws;
   a.delta = (float*)(wb + w.o_delta);
+  a.lse2 = (float*)(wb + w.o_lse2);
   a.part_dq = (float*)(wb + w.o_part_dq);
   a.part_dk = (float*)(wb + w.o_part_dk);
   a.part_dv = (float*)(wb + w.o_part_dv);
@@ -729,7 +736,7 @@ psattn_status psattn_tree_plan_array(const psattn_tree* t, int which, const int3
     case 2: *data = t->kv_list.data(); *count = (int64_t)t->kv_list.size(); *width = 1; break;
     case 3: *data = (const int32_t*)t->fwd.data(); *count = (int64_t)t->fwd.size(); *width = 8; break;
     case 4: *data = (const int32_t*)t->merge.data(); *count = (int64_t)t->merge.size(); *width = 4; break;
-    case 5: *data = (const int32_t*)t->bkv.data(); *count = (int64_t)t->bkv.size(); *width = 8; break;
+    case 5: *data = (const int32_t*)t->bkv.data(); *count = (int64_t)t->bkv.size(); *width = 10; break;
     case 6: *data = (const int32_t*)t->reduce.data(); *count = (int64_t)t->reduce.size(); *width = 8; break;
     case 7: *data = t->pad_slots.data(); *count = (int64_t)t->pad_slots.size(); *width = 1; break;
     default: return fail(PSATTN_E_INVALID_ARG, "unknown plan array %d", which);

@@ -33,6 +33,7 @@ struct BwdArgs {
   float* dK;
   float* dV;
   float* delta;    // [Hq][Ns]
+  float* lse2;     // [Hq][Ns] LSE * log2(e)
   float* part_dq;  // [partial rows][Hq][d]
   float* part_dk;  // [partial tiles][BKV_TILE][d]; each tile belongs to one kv head
   float* part_dv;

@@ -5,8 +5,11 @@
 //     its key range) x the node's root-to-node key path x a chunk of query
 //     heads that read one kv head;
 //   * dK/dV items: a tile of keys of one node x one kv head x a chunk of the
-//     rows that consume those keys (the node's own later rows, then every
-//     row of every descendant node -- all branches reusing the prefix);
+//     rows that consume those keys: every row of every descendant node (all
+//     branches reusing the prefix), then the node's own rows from its last
+//     position down to the tile's first key.  All tiles of a node therefore
+//     read the same rows in the same order, and their concurrent workgroups
+//     share those rows in L2;
 //   * fixed-order merge/reduce lists for items whose results are split.
 // Keys are addressed through per-path lists of pool slots, so a key tile
 // can straddle page blocks of any size.
@@ -44,7 +47,9 @@ struct BkvItem {
   int32_t nq;        // consumer rows in this chunk
   int32_t hk;        // kv head
   int32_t part;      // -1: write dK/dV directly; else partial tile index
-  int32_t nmask;     // leading rows of the chunk that may see only part of the keys
+  int32_t mask_lo;   // chunk rows [mask_lo, mask_hi) may see only part of the keys;
+  int32_t mask_hi;   //   every other row sees all of them
+  int32_t pad_;
 };
 
 struct ReduceEntry {  // a key tile whose consumer rows were split into chunks

@@ -213,12 +213,12 @@ def _check_plan(wl, t):
 
     # dK/dV items: every visible pair once per query head (G heads per kv head)
     cover = {}
-    for kv_off, nk, kv_pos0, q_off, nq, hk, part, nmask in bkv:
+    for kv_off, nk, kv_pos0, q_off, nq, hk, part, mask_lo, mask_hi, _ in bkv:
         keys = [slot_to_row[int(s)] for s in kv_list[kv_off:kv_off + nk]]
         rows = q_list[q_off:q_off + nq]
         for i, r in enumerate(rows):
-            if i >= nmask:
-                assert row_pos[r] >= kv_pos0 + nk - 1, "row past nmask sees only part of the tile"
+            if not (mask_lo <= i < mask_hi):
+                assert row_pos[r] >= kv_pos0 + nk - 1, "row outside the mask range sees only part of the tile"
             for j, k in enumerate(keys):
                 vis = (r, k) in visible
                 if row_pos[r] >= kv_pos0 + j:
