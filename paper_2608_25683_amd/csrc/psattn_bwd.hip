@@ -239,8 +239,8 @@ __global__ __launch_bounds__(512) void bwd_kv_bf16_kernel(BwdArgs a) {
   }
 }
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void bwd_dq_bf16_kernel(BwdArgs a) {
+template <int D, int NW, int NS>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void bwd_dq_bf16_kernel(BwdArgs a) {
   constexpr int RB = D * 2;
   constexpr int CPR = D / 8;
   constexpr int RPI = 64 / CPR;
@@ -249,7 +249,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_bf16_kernel(BwdArgs a) {
   constexpr int IPW = (NI + NW - 1) / NW;
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int TPB = IDX_BLK / KV_TILE;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2][2][TB];   // [stage][K | V]
+  constexpr int CPW = 2 * (NI / NW);          // K+V copies every wave issues per tile (at least)
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];   // [stage][K | V]
   __shared__ int s_slot[2][IDX_BLK];
 
   const FwdItem it = a.plan.fwd[blockIdx.x];
@@ -307,8 +308,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_bf16_kernel(BwdArgs a) {
         const int key = min(t * KV_TILE + r, nkv - 1);
         const int slot = s_slot[(key / IDX_BLK) & 1][key % IDX_BLK];
         const size_t go = (size_t)slot * kv_stride + ((cpc ^ swz<D>(r)) << 3);
-        copy16_to_lds(Kb + go, &smem[t & 1][0][k * 1024]);
-        copy16_to_lds(Vb + go, &smem[t & 1][1][k * 1024]);
+        copy16_to_lds(Kb + go, &smem[t % NS][0][k * 1024]);
+        copy16_to_lds(Vb + go, &smem[t % NS][1][k * 1024]);
       }
     }
   };
@@ -320,20 +321,27 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_bf16_kernel(BwdArgs a) {
 
   wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
   __syncthreads();
-  issue(0);
+  // NS-stage ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed.  Index blocks
+  // (TPB tiles each) are double-buffered in LDS; block b+1 is fetched into registers when tile
+  // TPB*b starts issuing and stored just before its first tile is issued.
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < ntiles) issue(p);
   for (int t = 0; t < ntiles; ++t) {
-    const int tn = t + 1;
+    const int tn = t + NS - 1;                 // tile issued in this iteration
     if (tn < ntiles && tn % TPB == 0 && tid < IDX_BLK) s_slot[(tn / TPB) & 1][tid] = pre;
-    wait_vmem<0>();
+    // this wave's copies for tile t are done once at most CPW*(NS-2) newer copies are in flight
+    if (t + NS - 2 < ntiles) wait_vmem<CPW * (NS - 2)>();
+    else wait_vmem<0>();
     __syncthreads();
     if (tn < ntiles) {
       issue(tn);
       if (tn % TPB == 0 && tid < IDX_BLK && (tn / TPB + 1) * IDX_BLK < nkv)
-        pre = kvl[min((tn / TPB + 1) * IDX_BLK + tid, nkv - 1)];
+        pre = load_untracked(kvl + min((tn / TPB + 1) * IDX_BLK + tid, nkv - 1));
     }
 
-    const uint8_t* Kt = &smem[t & 1][0][0];
-    const uint8_t* Vt = &smem[t & 1][1][0];
+    const uint8_t* Kt = &smem[t % NS][0][0];
+    const uint8_t* Vt = &smem[t % NS][1][0];
     f32x16 S[2], dP[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -345,19 +353,20 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_bf16_kernel(BwdArgs a) {
         dP[b] = mfma(as_bf(ld16(Vt + 32 * b * RB + koff[s])), doreg[s], dP[b]);
       }
     }
-    const bool need_mask = t >= it.nfull;
     // accumulator layout: lane <-> query row (column), element v <-> key 32*b + 8*(v/4) + 4*hh + v%4
+    if (t >= it.nfull) {   // wave-uniform: keys past the range or after the row get probability 0
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kidx = t * KV_TILE + 32 * b + 8 * (v >> 2) + 4 * hh + (v & 3);
+          if (kidx >= nkv || it.kv_pos0 + kidx > qpos) S[b][v] = kNegInf;
+        }
+    }
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float p = fast_exp2(fmaf(S[b][v], c, -lse2));
-        if (need_mask) {
-          const int kidx = t * KV_TILE + 32 * b + 8 * (v >> 2) + 4 * hh + (v & 3);
-          if (kidx >= nkv || it.kv_pos0 + kidx > qpos) p = 0.f;
-        }
-        dP[b][v] = p * (dP[b][v] - del);
-      }
+      for (int v = 0; v < 16; ++v) dP[b][v] = fast_exp2(fmaf(S[b][v], c, -lse2)) * (dP[b][v] - del);
     bf16x8 sb[2][2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -626,6 +635,7 @@ __global__ __launch_bounds__(256) void bwd_zero_pad_kernel(BwdArgs a) {
 
 #define PSATTN_NW_SWITCH(NW, BODY)                  \
   switch (NW) {                                     \
+    case 4: { constexpr int W_ = 4; BODY; } break;  \
     case 5: { constexpr int W_ = 5; BODY; } break;  \
     case 6: { constexpr int W_ = 6; BODY; } break;  \
     case 7: { constexpr int W_ = 7; BODY; } break;  \
@@ -659,9 +669,9 @@ hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st) {
   if (bf16) {
     const dim3 block(a.s.nw * 64);
     if (a.s.d == 128) {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<128, W_>), grid, block, 0, st, a));
+      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<128, W_, 2>), grid, block, 0, st, a));
     } else {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, W_>), grid, block, 0, st, a));
+      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, W_, 2>), grid, block, 0, st, a));
     }
   } else {
     const dim3 block(2 * a.s.bmq * a.s.hc);

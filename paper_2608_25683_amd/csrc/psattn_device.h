@@ -86,6 +86,15 @@ __device__ __forceinline__ void copy4_to_lds(const void* g, void* lds_base) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)PSATTN_LDS(void, lds_base));
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
+// Load one dword into a register without the compiler tracking its completion.  Used for
+// prefetches consumed several pipeline steps later: the kernels' own wait_vmem calls in between
+// guarantee the load has landed before the register is read.
+__device__ __forceinline__ int load_untracked(const int* p) {
+  int v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+
 // Wait until at most N vector-memory loads of this wave are in flight (gfx9 s_waitcnt encoding:
 // vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).  The intrinsic keeps
 // the compiler's own load scoreboard in step, so it inserts no further waits for older loads.

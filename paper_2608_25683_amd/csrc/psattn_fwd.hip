@@ -19,8 +19,8 @@ namespace {
 
 using namespace dev;
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(FwdArgs a) {
+template <int D, int NW, int NS>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int RB = D * 2;                      // bytes per tile row
   constexpr int CPR = D / 8;                     // 16-byte chunks per row
   constexpr int RPI = 64 / CPR;                  // rows per 64-lane copy instruction
@@ -30,7 +30,8 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int KS = D / 16;                     // k-steps over head_dim
   constexpr int DB = D / 32;                     // 32-wide head_dim blocks of O
   constexpr int TPB = IDX_BLK / KV_TILE;         // key tiles per staged index block
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2][2][TB];   // [stage][K | V]
+  constexpr int CPW = 2 * (NI / NW);          // K+V copies every wave issues per tile (at least)
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];   // [stage][K | V]
   __shared__ int s_slot[2][IDX_BLK];
 
   const FwdItem it = a.plan.fwd[blockIdx.x];
@@ -77,8 +78,8 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(FwdArgs a) {
   const bf16_t* Vb = (const bf16_t*)a.V + (size_t)hk * D;
   const int crow = lane / CPR, cpc = lane % CPR;
   auto issue = [&](int t) {
-    uint8_t* kdst = &smem[t & 1][0][0];
-    uint8_t* vdst = &smem[t & 1][1][0];
+    uint8_t* kdst = &smem[t % NS][0][0];
+    uint8_t* vdst = &smem[t % NS][1][0];
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const int k = wave + NW * i;
@@ -102,20 +103,27 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(FwdArgs a) {
 
   wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
   __syncthreads();
-  issue(0);
+  // NS-stage ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed.  Index blocks
+  // (TPB tiles each) are double-buffered in LDS; block b+1 is fetched into registers when tile
+  // TPB*b starts issuing and stored just before its first tile is issued.
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < ntiles) issue(p);
   for (int t = 0; t < ntiles; ++t) {
-    const int tn = t + 1;
+    const int tn = t + NS - 1;                 // tile issued in this iteration
     if (tn < ntiles && tn % TPB == 0 && tid < IDX_BLK) s_slot[(tn / TPB) & 1][tid] = pre;
-    wait_vmem<0>();
+    // this wave's copies for tile t are done once at most CPW*(NS-2) newer copies are in flight
+    if (t + NS - 2 < ntiles) wait_vmem<CPW * (NS - 2)>();
+    else wait_vmem<0>();
     __syncthreads();
     if (tn < ntiles) {
       issue(tn);
       if (tn % TPB == 0 && tid < IDX_BLK && (tn / TPB + 1) * IDX_BLK < nkv)
-        pre = kvl[min((tn / TPB + 1) * IDX_BLK + tid, nkv - 1)];
+        pre = load_untracked(kvl + min((tn / TPB + 1) * IDX_BLK + tid, nkv - 1));
     }
 
-    const uint8_t* Kt = &smem[t & 1][0][0];
-    const uint8_t* Vt = &smem[t & 1][1][0];
+    const uint8_t* Kt = &smem[t % NS][0][0];
+    const uint8_t* Vt = &smem[t % NS][1][0];
     f32x16 sacc[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -324,6 +332,7 @@ __global__ __launch_bounds__(256) void fwd_merge_kernel(FwdArgs a) {
 
 #define PSATTN_NW_SWITCH(NW, BODY)                  \
   switch (NW) {                                     \
+    case 4: { constexpr int W_ = 4; BODY; } break;  \
     case 5: { constexpr int W_ = 5; BODY; } break;  \
     case 6: { constexpr int W_ = 6; BODY; } break;  \
     case 7: { constexpr int W_ = 7; BODY; } break;  \
@@ -336,9 +345,9 @@ hipError_t launch_fwd_main(const FwdArgs& a, bool bf16, hipStream_t st) {
   if (bf16) {
     const dim3 block(a.s.nw * 64);
     if (a.s.d == 128) {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<128, W_>), grid, block, 0, st, a));
+      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<128, W_, 2>), grid, block, 0, st, a));
     } else {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<64, W_>), grid, block, 0, st, a));
+      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<64, W_, 2>), grid, block, 0, st, a));
     }
   } else {
     const dim3 block(2 * a.s.bmq * a.s.hc);  // two lanes per (row, head)

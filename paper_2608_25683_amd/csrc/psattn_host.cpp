@@ -230,7 +230,8 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   s.hc = 1;
   for (int c = 8; c >= 1; --c)
     if (s.g % c == 0) { s.hc = c; break; }
-  // 32-row subtiles per head: a forward/dQ workgroup holds up to 8 wavefronts (hc x rw)
+  // 32-row subtiles per head: a forward/dQ workgroup holds up to 8 wavefronts (hc x rw), so
+  // each staged key tile serves up to 8 x 32 query-head rows
   s.rw = (8 % s.hc == 0) ? 8 / s.hc : (s.hc <= 4 ? 2 : 1);
   s.nw = s.hc * s.rw;
   s.bmq = Q_SUB * s.rw;
