@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample (0 disables the cpu_baseline leg)")
     ap.add_argument("--no-profile", action="store_true", help="do not bracket kernels with timing events")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run two plain device copies of this many MiB (counter calibration) and exit")
     return ap.parse_args()
 
 
@@ -64,7 +66,12 @@ def kernel_traffic(kernel, config):
 
 
 def cpu_baseline(wl, seconds):
-    """The fp64 oracle, as it stands, on a bounded sample of the same workload (host cores)."""
+    """The fp64 oracle, as it stands, on a bounded sample of the same workload (host cores).
+
+    Runs the oracle's per-sample, per-head causal forward + backward over the workload's samples
+    in order, head by head, until about ``seconds`` of CPU time have passed; throughput counts
+    unshared-equivalent tokens (one sample token over all Hq heads = one token).
+    """
     import numpy as np
     import oracle as O
     try:
@@ -73,27 +80,43 @@ def cpu_baseline(wl, seconds):
     except Exception:
         threads = len(os.sched_getaffinity(0))
     t = wl.tree
-    rows = O.sample_rows(t.parent, t.seg_len, t.row_off, t.sample_end)
-    s = 0
-    idx = rows[s]
     G = wl.hq // wl.hkv
-    heads_done = 0
+    done = []   # (sample, heads)
+    tokens = 0.0
     t0 = time.perf_counter()
-    for h in range(wl.hq):
-        q = wl.Q[idx, h].astype(np.float64)
-        k = wl.K[idx, h // G].astype(np.float64)
-        v = wl.V[idx, h // G].astype(np.float64)
-        do = wl.dO[idx, h].astype(np.float64)
-        o, lse = O.causal_fwd(q, k, v, wl.scale)
-        O.causal_bwd(q, k, v, o, lse, do, wl.scale)
-        heads_done += 1
+    for s, idx in enumerate(O.sample_rows(t.parent, t.seg_len, t.row_off, t.sample_end)):
+        heads = 0
+        for h in range(wl.hq):
+            q = wl.Q[idx, h].astype(np.float64)
+            k = wl.K[idx, h // G].astype(np.float64)
+            v = wl.V[idx, h // G].astype(np.float64)
+            do = wl.dO[idx, h].astype(np.float64)
+            o, lse = O.causal_fwd(q, k, v, wl.scale)
+            O.causal_bwd(q, k, v, o, lse, do, wl.scale)
+            heads += 1
+            tokens += len(idx) / wl.hq
+            if time.perf_counter() - t0 >= seconds:
+                break
+        done.append((s, len(idx), heads))
         if time.perf_counter() - t0 >= seconds:
             break
     el = time.perf_counter() - t0
-    tokens = len(idx) * heads_done / wl.hq      # unshared-equivalent tokens (all Hq heads = 1 token)
+    desc = "; ".join(f"sample {s} ({n} tokens) x {h} heads" for s, n, h in done)
     return {"value": tokens / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"sample 0 ({len(idx)} tokens) x {heads_done} of {wl.hq} query heads, fwd+bwd, fp64 numpy; "
-                      f"{el:.1f} s wall"}
+            "sample": f"{desc} of {wl.hq} query heads each, fwd+bwd, fp64 numpy; {el:.1f} s wall"}
+
+
+def copy_calibration(mib):
+    """A plain device-to-device copy of known size, to scale the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = mib * (1 << 20) // 2
+    x = torch.ones(n, dtype=torch.bfloat16, device="cuda:0")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 2, "copy_calibration_bytes_written": n * 2}), flush=True)
 
 
 def main():
@@ -102,6 +125,9 @@ def main():
         print("bench.py runs on one GPU only: the prefix-shared attention path is a single-GPU kernel "
               "(multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
         sys.exit(2)
+    if a.copy_calibration_mib:
+        copy_calibration(a.copy_calibration_mib)
+        return
     import numpy as np
     import torch
     from paper_2608_25683_amd import workloads as W
