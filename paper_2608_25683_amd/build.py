@@ -26,8 +26,20 @@ def _run(cmd):
     return out
 
 
+def check_hazards(src, extra_flags=None) -> None:
+    """Compiles the device code of one source to assembly and runs the MFMA hazard check on it."""
+    from . import hazard_check
+    asm = os.path.join(PKG, "_build", os.path.splitext(src)[0] + ".s")
+    _run([HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS,
+          *(extra_flags or []), "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", asm])
+    bad = {k: v for k, v in hazard_check.check_file(asm).items() if v}
+    if bad:
+        lines = [f"{k}: {len(v)} violations, first: {v[0]}" for k, v in bad.items()]
+        raise RuntimeError("MFMA hazard check failed for " + src + ":\n" + "\n".join(lines))
+
+
 def build(verbose: bool = False, extra_flags=None) -> str:
-    """Compile every source for gfx950 and link the shared library; returns its path."""
+    """Compile every source for gfx950, check the kernels' MFMA hazards, link; returns the path."""
     objs = []
     os.makedirs(os.path.join(PKG, "_build"), exist_ok=True)
     for src in SOURCES:
@@ -41,6 +53,8 @@ def build(verbose: bool = False, extra_flags=None) -> str:
         if verbose and out.strip():
             print(out)
         objs.append(obj)
+        if src.endswith(".hip"):
+            check_hazards(src, extra_flags)
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)

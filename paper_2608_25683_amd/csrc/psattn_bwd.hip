@@ -250,6 +250,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int TPB = IDX_BLK / KV_TILE;
   constexpr int CPW = 2 * (NI / NW);          // K+V copies every wave issues per tile (at least)
+  static_assert(NS - 1 <= TPB, "index blocks are fetched once per TPB tiles");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];   // [stage][K | V]
   __shared__ int s_slot[2][IDX_BLK];
 
@@ -269,9 +270,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int* kvl = a.plan.kv_list + it.kv_off;
   const int ntiles = (nkv + KV_TILE - 1) / KV_TILE;
 
-  if (tid < IDX_BLK) s_slot[0][tid] = kvl[min(tid, nkv - 1)];
-  int pre = 0;
-  if (tid < IDX_BLK && nkv > IDX_BLK) pre = kvl[min(IDX_BLK + tid, nkv - 1)];
+  if (tid < IDX_BLK) {
+    s_slot[0][tid] = kvl[min(tid, nkv - 1)];
+    if (nkv > IDX_BLK) s_slot[1][tid] = kvl[min(IDX_BLK + tid, nkv - 1)];
+  }
 
   bf16x8 qreg[KS], doreg[KS];
   {
@@ -314,6 +316,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
   };
 
+  // index block b (entries IDX_BLK*b ...) into its LDS buffer, one dword per lane
+  auto fetch_index_block = [&](int b) {
+    if (b * IDX_BLK >= nkv) return;
+    for (int w = wave; w < IDX_BLK / 64; w += NW)
+      copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
+  };
+
   f32x16 dq[DB];
 #pragma unroll
   for (int mb = 0; mb < DB; ++mb) dq[mb] = f32x16{};
@@ -322,22 +331,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
   __syncthreads();
   // NS-stage ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed.  Index blocks
-  // (TPB tiles each) are double-buffered in LDS; block b+1 is fetched into registers when tile
-  // TPB*b starts issuing and stored just before its first tile is issued.
+  // (TPB tiles each) are double-buffered in LDS: blocks 0 and 1 are loaded up front, and block
+  // b+1 is copied global -> LDS when tile TPB*b is issued, into the buffer of block b-1, whose
+  // tiles have all been issued by then.  The waits before later tiles cover that copy.
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
     if (p < ntiles) issue(p);
   for (int t = 0; t < ntiles; ++t) {
     const int tn = t + NS - 1;                 // tile issued in this iteration
-    if (tn < ntiles && tn % TPB == 0 && tid < IDX_BLK) s_slot[(tn / TPB) & 1][tid] = pre;
     // this wave's copies for tile t are done once at most CPW*(NS-2) newer copies are in flight
     if (t + NS - 2 < ntiles) wait_vmem<CPW * (NS - 2)>();
     else wait_vmem<0>();
     __syncthreads();
     if (tn < ntiles) {
       issue(tn);
-      if (tn % TPB == 0 && tid < IDX_BLK && (tn / TPB + 1) * IDX_BLK < nkv)
-        pre = load_untracked(kvl + min((tn / TPB + 1) * IDX_BLK + tid, nkv - 1));
+      if (tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
     }
 
     const uint8_t* Kt = &smem[t % NS][0][0];

@@ -20,6 +20,25 @@ typedef __attribute__((ext_vector_type(2))) float f32x2;
 
 #define PSATTN_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
 
+// compile-time flag passed to generic lambdas (if constexpr on decltype(flag)::value)
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
+
+// compile-time integer, and a loop that calls f(IntC<0>{}) .. f(IntC<N-1>{}) (fully unrolled)
+template <int I>
+struct IntC {
+  static constexpr int value = I;
+};
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IntC<I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 constexpr int IDX_BLK = 256;   // slot / row indices staged in LDS per block
@@ -81,20 +100,22 @@ __device__ __forceinline__ void copy16_to_lds(const void* g, void* lds_base) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)PSATTN_LDS(void, lds_base));
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
+// As copy16_to_lds, with the LDS byte address given directly (wave-uniform).
+__device__ __forceinline__ void copy16_to_lds_at(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+// As copy16_to_lds_at, reading 16 bytes at base + off for each lane (base wave-uniform, off a
+// 32-bit byte offset per lane).
+__device__ __forceinline__ void copy16_to_lds_off(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+// LDS byte address of a pointer into a __shared__ array (the low half of its generic address).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 // 4 bytes per lane: lane i writes lds_base + 4 i (inactive lanes write nothing).
 __device__ __forceinline__ void copy4_to_lds(const void* g, void* lds_base) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)PSATTN_LDS(void, lds_base));
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
-// Load one dword into a register without the compiler tracking its completion.  Used for
-// prefetches consumed several pipeline steps later: the kernels' own wait_vmem calls in between
-// guarantee the load has landed before the register is read.
-__device__ __forceinline__ int load_untracked(const int* p) {
-  int v;
-  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-  return v;
-}
-
 // Wait until at most N vector-memory loads of this wave are in flight (gfx9 s_waitcnt encoding:
 // vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).  The intrinsic keeps
 // the compiler's own load scoreboard in step, so it inserts no further waits for older loads.
@@ -103,6 +124,72 @@ __device__ __forceinline__ void wait_vmem() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+
+// ---- MFMA through inline assembly, with the register class of each operand chosen here
+// (accumulators and loop-invariant operands in AGPRs, scores in VGPRs).  The compiler does not
+// treat these as matrix instructions, so the data hazards it would otherwise resolve are the
+// caller's: a non-MFMA instruction may read or overwrite an MFMA result only 12 wait states after
+// the MFMA that wrote it (see mfma_fence_a), and a register written by a VALU instruction may
+// feed an MFMA only 2 wait states later.  Chained accumulation into the same registers needs
+// no wait.
+// d = a * b, d in VGPRs, b in AGPRs
+__device__ __forceinline__ void mma_v_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(b));
+}
+// d += a * b, d in VGPRs, b in AGPRs
+__device__ __forceinline__ void mma_v(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
+}
+// d = a * b and d += a * b with d and b in AGPRs
+__device__ __forceinline__ void mma_aa_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&a"(d) : "v"(a), "a"(b));
+}
+__device__ __forceinline__ void mma_aa(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(d) : "v"(a), "a"(b));
+}
+// d += a * b, d in AGPRs, a and b in VGPRs
+__device__ __forceinline__ void mma_a(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(d) : "v"(a), "v"(b));
+}
+// Keep x in AGPRs from here on (an AGPR operand of the MFMAs above).
+__device__ __forceinline__ void pin_a(bf16x8& x) { asm volatile("" : "+a"(x)); }
+__device__ __forceinline__ void pin_a(f32x16& x) { asm volatile("" : "+a"(x)); }
+// 12 wait states before later instructions may touch the results of the MFMAs issued so far;
+// the accumulators passed to the following pin_a calls are then ordered after the wait.
+__device__ __forceinline__ void mfma_fence() { asm volatile("s_nop 11"); }
+// 2 wait states after VALU writes, before MFMAs read them.
+__device__ __forceinline__ void valu_fence() { asm volatile("s_nop 1"); }
+// Plain IEEE max without the quieting of signalling NaNs that fmaxf implies for operands the
+// compiler cannot see the origin of (MFMA results from inline assembly).
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float max2f(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+// acc + lo + hi of a packed bf16 pair (one v_dot2c_f32_bf16 against (1, 1))
+__device__ __forceinline__ float add_bf16_pair(uint32_t pair, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pair), one, acc, false);
+}
+// max over the lane pair (l, l ^ 32)
+__device__ __forceinline__ float pair_max2(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max2f(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Materialize x here: its computation cannot sink past this point.
+__device__ __forceinline__ void anchor(float& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void anchor(f32x16& x) { asm volatile("" : "+v"(x)); }
+// Move x to VGPRs here (from AGPRs, if it lives there).
+__device__ __forceinline__ void pin_v(f32x16& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void anchor(bf16x8& x) { asm volatile("" : "+v"(x)); }
+// Keep the scheduler from moving any instruction across this point.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Transposing LDS read: within each 16-lane group, lanes 4r..4r+3 point at 4 consecutive bf16 of
 // row r (r = 0..3) and lane i of the group receives column i of those 4 rows.

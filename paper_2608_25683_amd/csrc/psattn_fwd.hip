@@ -14,6 +14,13 @@
 // by more than 2^8, so O and the row sum are rarely rescaled.
 #include "psattn_device.h"
 
+#ifndef PSATTN_FWD_NS
+#define PSATTN_FWD_NS 4
+#endif
+#ifndef PSATTN_FWD_PF
+#define PSATTN_FWD_PF 4
+#endif
+
 namespace psattn {
 namespace {
 
@@ -31,6 +38,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   constexpr int DB = D / 32;                     // 32-wide head_dim blocks of O
   constexpr int TPB = IDX_BLK / KV_TILE;         // key tiles per staged index block
   constexpr int CPW = 2 * (NI / NW);          // K+V copies every wave issues per tile (at least)
+  static_assert(NS - 1 <= TPB, "index blocks are fetched once per TPB tiles");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];   // [stage][K | V]
   __shared__ int s_slot[2][IDX_BLK];
 
@@ -48,9 +56,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int* kvl = a.plan.kv_list + it.kv_off;
   const int ntiles = (nkv + KV_TILE - 1) / KV_TILE;
 
-  if (tid < IDX_BLK) s_slot[0][tid] = kvl[min(tid, nkv - 1)];
-  int pre = 0;
-  if (tid < IDX_BLK && nkv > IDX_BLK) pre = kvl[min(IDX_BLK + tid, nkv - 1)];
+  if (tid < IDX_BLK) {
+    s_slot[0][tid] = kvl[min(tid, nkv - 1)];
+    if (nkv > IDX_BLK) s_slot[1][tid] = kvl[min(IDX_BLK + tid, nkv - 1)];
+  }
 
   bf16x8 qreg[KS];
   {
@@ -94,6 +103,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
   };
 
+  // index block b (entries IDX_BLK*b ...) into its LDS buffer, one dword per lane
+  auto fetch_index_block = [&](int b) {
+    if (b * IDX_BLK >= nkv) return;
+    for (int w = wave; w < IDX_BLK / 64; w += NW)
+      copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
+  };
+
   f32x16 oacc[DB];
 #pragma unroll
   for (int mb = 0; mb < DB; ++mb) oacc[mb] = f32x16{};
@@ -104,22 +120,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
   __syncthreads();
   // NS-stage ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed.  Index blocks
-  // (TPB tiles each) are double-buffered in LDS; block b+1 is fetched into registers when tile
-  // TPB*b starts issuing and stored just before its first tile is issued.
+  // (TPB tiles each) are double-buffered in LDS: blocks 0 and 1 are loaded up front, and block
+  // b+1 is copied global -> LDS when tile TPB*b is issued, into the buffer of block b-1, whose
+  // tiles have all been issued by then.  The waits before later tiles cover that copy.
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
     if (p < ntiles) issue(p);
   for (int t = 0; t < ntiles; ++t) {
     const int tn = t + NS - 1;                 // tile issued in this iteration
-    if (tn < ntiles && tn % TPB == 0 && tid < IDX_BLK) s_slot[(tn / TPB) & 1][tid] = pre;
     // this wave's copies for tile t are done once at most CPW*(NS-2) newer copies are in flight
     if (t + NS - 2 < ntiles) wait_vmem<CPW * (NS - 2)>();
     else wait_vmem<0>();
     __syncthreads();
     if (tn < ntiles) {
       issue(tn);
-      if (tn % TPB == 0 && tid < IDX_BLK && (tn / TPB + 1) * IDX_BLK < nkv)
-        pre = load_untracked(kvl + min((tn / TPB + 1) * IDX_BLK + tid, nkv - 1));
+      if (tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
     }
 
     const uint8_t* Kt = &smem[t % NS][0][0];
@@ -209,6 +224,394 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
         *(f32x4*)(op + 32 * mb + 8 * g4 + 4 * hh) =
             f32x4{oacc[mb][4 * g4] * inv, oacc[mb][4 * g4 + 1] * inv, oacc[mb][4 * g4 + 2] * inv, oacc[mb][4 * g4 + 3] * inv};
     if (hh == 0) a.part_lse[prow * a.s.hq + head] = lse;
+  }
+}
+
+// ============================================================================================
+// bf16 main kernel, 64 rows per wavefront.  One wavefront per SIMD (up to 512 registers), so a
+// wave holds the queries (AGPRs), the output accumulators (AGPRs) and the scores (VGPRs) of 64
+// rows -- two 32-row halves -- of one head: every K or V fragment read from LDS feeds two MFMAs,
+// half the LDS traffic per flop of a 32-row wave.  Work proceeds in 32-key blocks j; stage j
+// issues the score MFMAs of block j+1 and the PV MFMAs of block j-1, and between them the
+// softmax of block j (its scores were finished during stage j-1).  The instruction order inside
+// a stage is fixed (scheduling fences), so the VALU softmax runs in the shadow of the MFMAs.
+// Key tiles (two blocks) come through an NS-stage LDS ring, one barrier per tile.
+template <int D, int NW, int NS>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_bf16_w64_kernel(FwdArgs a) {
+  constexpr int RB = D * 2;
+  constexpr int CPR = D / 8;
+  constexpr int RPI = 64 / CPR;
+  constexpr int TB = KV_TILE * RB;
+  constexpr int NI = KV_TILE / RPI;
+  constexpr int IPW = NI / NW;
+  constexpr int KS = D / 16;                     // score MFMAs per row half and block
+  constexpr int DB = D / 32;
+  constexpr int NPV = 2 * DB;                    // PV MFMAs per row half and block
+  constexpr int TPB = IDX_BLK / KV_TILE;
+  constexpr int CPW = 2 * IPW;                   // K+V copies every wave issues per tile
+  static_assert(NI % NW == 0 && NS >= 3 && NS - 1 <= TPB, "tile copy split / ring depth");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];
+  __shared__ int s_slot[2][IDX_BLK];
+
+  const FwdItem it = a.plan.fwd[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int rw2 = a.s.rw >> 1;                   // 64-row blocks per head
+  const int head = it.head0 + wave / rw2;
+  const int hk = it.head0 / a.s.g;
+  const int nkv = it.nkv;
+  const int* kvl = a.plan.kv_list + it.kv_off;
+  const int ntiles = (nkv + KV_TILE - 1) / KV_TILE;
+
+  for (int i = tid; i < IDX_BLK; i += NW * 64) {
+    s_slot[0][i] = kvl[min(i, nkv - 1)];
+    if (nkv > IDX_BLK) s_slot[1][i] = kvl[min(IDX_BLK + i, nkv - 1)];
+  }
+
+  int ridx[2], row[2], lim[2];
+  bool row_ok[2];
+  bf16x8 qreg[2][KS];
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh) {
+    ridx[rh] = (wave % rw2) * 64 + 32 * rh + l32;
+    row_ok[rh] = ridx[rh] < it.nq;
+    row[rh] = a.plan.q_list[it.q_off + (row_ok[rh] ? ridx[rh] : it.nq - 1)];
+    // key kidx of this item is visible to the row iff kidx <= lim
+    lim[rh] = min(nkv - 1, a.plan.row_pos[row[rh]] - it.kv_pos0);
+    const bf16_t* qp = (const bf16_t*)a.Q + ((size_t)row[rh] * a.s.hq + head) * D + 8 * hh;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qreg[rh][s] = as_bf(ld16(qp + 16 * s));
+  }
+
+  // LDS byte offsets of this lane's fragments inside a K or V tile
+  const int koff0 = tile_off<D>(l32, hh);                  // K rows l32, chunk 2s + hh: koff0 ^ (s << 5)
+  int voff[2];                                             // V^T reads, d block mb: voff ^ (mb << 6)
+  {
+    const int r4 = (lane & 15) >> 2, j = lane & 3, dsub = 16 * ((lane >> 4) & 1);
+#pragma unroll
+    for (int rd = 0; rd < 2; ++rd) voff[rd] = tile_off<D>(8 * rd + 4 * hh + r4, (dsub + 4 * j) >> 3) + 8 * (j & 1);
+  }
+  static_assert(D == 128 || D == 64, "head_dim");
+
+  // pool rows are addressed by 32-bit byte offsets from the head's base (the launcher checks that
+  // the pools are under 4 GiB and 2^24 rows, so slot * kv_stride is one 24-bit multiply-add)
+  const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
+  const uint8_t* Kb = (const uint8_t*)a.K + (size_t)hk * D * sizeof(bf16_t);
+  const uint8_t* Vb = (const uint8_t*)a.V + (size_t)hk * D * sizeof(bf16_t);
+  const int crow = lane / CPR, cpc = lane % CPR;
+  const uint32_t smem_base = lds_addr(&smem[0][0][0]);
+  // copies of key tile t: slot lookups first (issue_slots), then IPW pairs of K and V copies
+  auto issue_slots = [&](int t, int (&slot)[IPW]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int key = min(t * KV_TILE + (wave + NW * i) * RPI + crow, nkv - 1);
+      slot[i] = s_slot[(key / IDX_BLK) & 1][key % IDX_BLK];
+    }
+  };
+  // copy instruction i of tile t into ring slot rs, K (tensor 0) or V (tensor 1)
+  auto issue_copy1 = [&](int rs, int i, int slot, int tensor) __attribute__((always_inline)) {
+    const int k = wave + NW * i;
+    const int r = k * RPI + crow;
+    const uint32_t dst = smem_base + (uint32_t)((rs * 2 + tensor) * TB) + k * 1024;
+    const uint32_t off = __umul24((uint32_t)slot, kv_stride) + ((cpc ^ swz<D>(r)) << 4);
+    copy16_to_lds_off(tensor ? Vb : Kb, off, dst);
+  };
+  // all copies into ring slot t % NS, of tile min(t, ntiles - 1): past the last tile a copy
+  // refills a slot no one reads, so every iteration issues the same copies and waits the same
+  auto issue = [&](int t) __attribute__((always_inline)) {
+    int slot[IPW];
+    issue_slots(min(t, ntiles - 1), slot);
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      issue_copy1(t % NS, i, slot[i], 0);
+      issue_copy1(t % NS, i, slot[i], 1);
+    }
+  };
+  auto fetch_index_block = [&](int b) __attribute__((always_inline)) {
+    if (b * IDX_BLK >= nkv) return;
+    for (int w = wave; w < IDX_BLK / 64; w += NW)
+      copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
+  };
+
+  f32x16 oacc[2][DB];
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+    for (int mb = 0; mb < DB; ++mb) {
+      oacc[rh][mb] = f32x16{};
+      pin_a(oacc[rh][mb]);
+    }
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+    for (int s = 0; s < KS; ++s) pin_a(qreg[rh][s]);
+  valu_fence();
+  float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
+  const float c = a.s.scale * kLog2e;
+  const float th = 8.f / c;
+
+  // ---- one stage.  Sc: scores of block j (softmax now, K rows at Kc); Sn: scores of block
+  // j+1 (MFMAs now, K rows at Kn); Pp: probabilities of block j-1 (PV MFMAs now, V rows at Vp);
+  // Pc: block j's probabilities (written).  extra(IntC<i>) runs after MFMA slot i.
+  //
+  // The softmax exponentiates against the running max of the earlier blocks while block j's
+  // own row max is reduced alongside, so no exponential waits for a reduction.  A row whose max
+  // grows by more than 2^8 (always the case for the first block of a row) sends the whole wave
+  // down a slow path after the stage: block j's scores are recomputed from Kc, exponentiated
+  // against the new max, and O and the running sum are rescaled.
+  auto scores = [&](const uint8_t* Kb_, f32x16 (&S)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const bf16x8 k = as_bf(ld16(Kb_ + (koff0 ^ (s << 5))));
+#pragma unroll
+      for (int rh = 0; rh < 2; ++rh) {
+        if (s == 0) mma_v_first(S[rh], k, qreg[rh][s]);
+        else mma_v(S[rh], k, qreg[rh][s]);
+      }
+    }
+  };
+  auto mask_elem = [&](f32x16 (&S)[2], int rh, int v, int kb) __attribute__((always_inline)) {
+    // element v holds key kb + 4*hh + 8*(v/4) + v%4, visible iff it is <= lim
+    const int x = lim[rh] - kb - 4 * hh;
+    S[rh][v] = (8 * (v >> 2) + (v & 3) > x) ? kNegInf : S[rh][v];
+  };
+  auto stage = [&](f32x16 (&Sc)[2], f32x16 (&Sn)[2], const bf16x8 (&Pp)[2][2], bf16x8 (&Pc)[2][2],
+                   const uint8_t* Kc, const uint8_t* Kn, const uint8_t* Vp, int kb, auto masked,
+                   auto extra, auto pv_first) __attribute__((always_inline)) {
+    float mx[2], mt[2], ps[2][2], l_prev[2], mc[2];
+    bool g[2];
+#pragma unroll
+    for (int rh = 0; rh < 2; ++rh) mc[rh] = m_run[rh] == kNegInf ? 0.f : m_run[rh] * c;
+    // element e = 16 rh + v is scaled at chunk F(e), exponentiated at F(e)+1, summed at F(e)+2
+    auto F = [](int e) constexpr { return (e * 29) / 32; };
+    auto chunk = [&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      if constexpr (q == 0) {
+        l_prev[0] = l_run[0];
+        l_prev[1] = l_run[1];
+      }
+      if constexpr (q < 8) {          // mask, then row max steps over elements 2q, 2q+1 of both halves
+#pragma unroll
+        for (int rh = 0; rh < 2; ++rh) {
+          if constexpr (decltype(masked)::value) {
+            mask_elem(Sc, rh, 2 * q, kb);
+            mask_elem(Sc, rh, 2 * q + 1, kb);
+          }
+          if constexpr (q == 0) mx[rh] = max2f(Sc[rh][0], Sc[rh][1]);
+          else mx[rh] = max3f(mx[rh], Sc[rh][2 * q], Sc[rh][2 * q + 1]);
+          anchor(mx[rh]);
+        }
+      }
+      if constexpr (q == 9) {
+#pragma unroll
+        for (int rh = 0; rh < 2; ++rh) {
+          mt[rh] = pair_max2(mx[rh]);
+          anchor(mt[rh]);
+        }
+      }
+      if constexpr (q == 11) {
+#pragma unroll
+        for (int rh = 0; rh < 2; ++rh) g[rh] = mt[rh] > m_run[rh] + th;
+      }
+      static_for<32>([&](auto ec) __attribute__((always_inline)) {
+        constexpr int e = decltype(ec)::value, rh = e / 16, v = e % 16;
+        if constexpr (F(e) == q) Sc[rh][v] = fmaf(Sc[rh][v], c, -mc[rh]);
+        if constexpr (F(e) + 1 == q) Sc[rh][v] = fast_exp2(Sc[rh][v]);
+        if constexpr (F(e) + 2 == q) {
+          if constexpr (v < 2) ps[rh][v] = Sc[rh][v];
+          else ps[rh][v & 1] += Sc[rh][v];
+          anchor(ps[rh][v & 1]);
+        }
+        if constexpr (v % 8 == 7 && F(e) + 2 == q) {
+          Pc[rh][v / 8] = pack8(Sc[rh], 8 * (v / 8));
+          anchor(Pc[rh][v / 8]);
+        }
+      });
+      if constexpr (q == 31) {
+#pragma unroll
+        for (int rh = 0; rh < 2; ++rh) {
+          l_run[rh] += ps[rh][0] + ps[rh][1];
+          anchor(l_run[rh]);
+        }
+      }
+    };
+    static_assert(F(31) + 2 <= 31, "softmax schedule");
+    bf16x8 kf[KS], vf[NPV];
+    auto load_k = [&](int s) __attribute__((always_inline)) { kf[s] = as_bf(ld16(Kn + (koff0 ^ (s << 5)))); };
+    auto load_v = [&](int u) __attribute__((always_inline)) {   // u = DB * t2 + mb
+      const int t2 = u / DB, mb = u % DB;
+      const uint8_t* vp = Vp + 16 * t2 * RB;
+      vf[u] = as_bf(lds_tr(vp + (voff[0] ^ (mb << 6))), lds_tr(vp + (voff[1] ^ (mb << 6))));
+    };
+    // fragments in use order (K fragments then V fragments, or V first when pv_first); each is
+    // read PF MFMA pairs ahead of the pair that consumes it
+    constexpr bool PVF = decltype(pv_first)::value;
+    constexpr int PF = PSATTN_FWD_PF;
+    auto load_frag = [&](int f) __attribute__((always_inline)) {
+      if (PVF) {
+        if (f < NPV) load_v(f);
+        else if (f < NPV + KS) load_k(f - NPV);
+      } else {
+        if (f < KS) load_k(f);
+        else if (f < KS + NPV) load_v(f - KS);
+      }
+    };
+#pragma unroll
+    for (int f = 0; f < PF; ++f) load_frag(f);
+    constexpr int NSLOT = 2 * KS + 2 * NPV;
+    auto slot = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      constexpr int iq = PVF ? (i >= 2 * NPV ? i - 2 * NPV : -1) : (i < 2 * KS ? i : -1);   // score slot index
+      constexpr int ip = PVF ? (i < 2 * NPV ? i : -1) : (i >= 2 * KS ? i - 2 * KS : -1);    // PV slot index
+      if constexpr (iq >= 0) {
+        constexpr int s = iq / 2, rh = iq % 2;
+        if constexpr (rh == 0) load_frag((PVF ? NPV : 0) + s + PF);
+        if constexpr (s == 0) mma_v_first(Sn[rh], kf[s], qreg[rh][s]);
+        else mma_v(Sn[rh], kf[s], qreg[rh][s]);
+      } else {
+        constexpr int u = ip / 2, rh = ip % 2;
+        constexpr int t2 = u / DB, mb = u % DB;
+        if constexpr (rh == 0) load_frag((PVF ? 0 : KS) + u + PF);
+        mma_a(oacc[rh][mb], vf[u], Pp[rh][t2]);
+      }
+      // softmax chunks [32 i / NSLOT, 32 (i+1) / NSLOT) follow slot i
+      static_for<(32 * (i + 1)) / NSLOT - (32 * i) / NSLOT>([&](auto dq) __attribute__((always_inline)) {
+        chunk(IntC<(32 * i) / NSLOT + decltype(dq)::value>{});
+      });
+      extra(ic);
+      sched_fence();
+    };
+    static_for<NSLOT>(slot);
+    if (__any(g[0] || g[1])) {
+      // slow path: new row maxima.  Recompute block j's scores (its K rows are still resident),
+      // exponentiate them against the new maxima, and rescale O and the running sums.
+      f32x16 R[2];
+      scores(Kc, R);
+      mfma_fence();
+#pragma unroll
+      for (int rh = 0; rh < 2; ++rh) {
+        pin_v(R[rh]);
+        const float m_new = g[rh] ? mt[rh] : m_run[rh];
+        const float alpha = (g[rh] && m_run[rh] != kNegInf) ? fast_exp2((m_run[rh] - m_new) * c) : 1.f;
+        m_run[rh] = m_new;
+        const float mcn = m_new == kNegInf ? 0.f : m_new * c;
+        float sum = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          if constexpr (decltype(masked)::value) mask_elem(R, rh, v, kb);
+          R[rh][v] = fast_exp2(fmaf(R[rh][v], c, -mcn));
+          sum += R[rh][v];
+        }
+        l_run[rh] = l_prev[rh] * alpha + sum;
+        Pc[rh][0] = pack8(R[rh], 0);
+        Pc[rh][1] = pack8(R[rh], 8);
+#pragma unroll
+        for (int mb = 0; mb < DB; ++mb) {
+          pin_a(oacc[rh][mb]);
+          oacc[rh][mb] *= alpha;
+        }
+      }
+    }
+  };
+  wait_vmem<0>();
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p) issue(p);
+  wait_vmem<CPW * (NS - 2)>();
+  __syncthreads();
+
+  f32x16 SA[2], SB[2];
+  bf16x8 PA[2][2], PB[2][2];
+  // block 0's scores; block -1's probabilities are zero (its PV products, on tile 0's V rows,
+  // add nothing)
+  scores(&smem[0][0][0], SA);
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) PB[rh][t2] = bf16x8{};
+  mfma_fence();
+
+  auto tile = [&](int t, auto masked) __attribute__((always_inline)) {
+    const uint8_t* Kt = &smem[t % NS][0][0];
+    const uint8_t* Vt = &smem[t % NS][1][0];
+    const uint8_t* Vprev = t > 0 ? &smem[(t + NS - 1) % NS][1][0] + 32 * RB : Vt;
+    const int tn = t + NS - 1;
+    int slot[IPW];
+    issue_slots(min(tn, ntiles - 1), slot);
+    // stage 2t: scores of block 2t+1, PV of block 2t-1, softmax of block 2t; K copies
+    auto kcopies = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (i % 4 == 2 && i / 4 < IPW) issue_copy1(tn % NS, i / 4, slot[i / 4], 0);
+    };
+    stage(SA, SB, PB, PA, Kt, Kt + 32 * RB, Vprev, t * KV_TILE, masked, kcopies, Flag<false>{});
+    // tile t+1 must be resident before its first block's scores: newer copies are K and V of
+    // tiles t+2 .. t+NS-2 and K of tile t+NS-1
+    wait_vmem<(2 * NS - 5) * IPW>();
+    __syncthreads();
+    // stage 2t+1: PV of block 2t first (V rows resident before the barrier), then the scores of
+    // block 2t+2 (K rows of tile t+1; unused past the last tile), softmax of 2t+1; V copies
+    auto vcopies = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (i % 4 == 2 && i / 4 < IPW) issue_copy1(tn % NS, i / 4, slot[i / 4], 1);
+      if constexpr (i == 4 * IPW + 2) {
+        if (tn < ntiles && tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
+      }
+    };
+    stage(SB, SA, PA, PB, Kt + 32 * RB, &smem[(t + 1) % NS][0][0], Vt, t * KV_TILE + 32, masked, vcopies, Flag<true>{});
+  };
+  int t = 0;
+  for (; t < min(it.nfull, ntiles); ++t) tile(t, Flag<false>{});
+  for (; t < ntiles; ++t) tile(t, Flag<true>{});
+  wait_vmem<0>();   // no copy may still be writing this workgroup's LDS when it ends
+  // PV of the last block
+  {
+    const uint8_t* Vl = &smem[(ntiles - 1) % NS][1][0] + 32 * RB;
+#pragma unroll
+    for (int u = 0; u < NPV; ++u) {
+      const int t2 = u / DB, mb = u % DB;
+      const uint8_t* vp = Vl + 16 * t2 * RB;
+      const bf16x8 v = as_bf(lds_tr(vp + (voff[0] ^ (mb << 6))), lds_tr(vp + (voff[1] ^ (mb << 6))));
+      mma_a(oacc[0][mb], v, PB[0][t2]);
+      mma_a(oacc[1][mb], v, PB[1][t2]);
+    }
+    mfma_fence();
+#pragma unroll
+    for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+      for (int mb = 0; mb < DB; ++mb) pin_a(oacc[rh][mb]);
+  }
+
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh) {
+    const float l_tot = pair_sum(l_run[rh]);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lse = l_tot > 0.f ? m_run[rh] * a.s.scale + logf(l_tot) : kNegInf;
+    if (!row_ok[rh]) continue;
+    if (it.part < 0) {
+      bf16_t* op = (bf16_t*)a.O + ((size_t)row[rh] * a.s.hq + head) * D;
+#pragma unroll
+      for (int mb = 0; mb < DB; ++mb)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          u32x2 w;
+          w[0] = pack2(oacc[rh][mb][4 * g4 + 0] * inv, oacc[rh][mb][4 * g4 + 1] * inv);
+          w[1] = pack2(oacc[rh][mb][4 * g4 + 2] * inv, oacc[rh][mb][4 * g4 + 3] * inv);
+          *(u32x2*)(op + 32 * mb + 8 * g4 + 4 * hh) = w;
+        }
+      if (hh == 0) a.LSE[(size_t)head * a.s.ns + row[rh]] = lse;
+    } else {
+      const size_t prow = (size_t)it.part + ridx[rh];
+      float* op = a.part_o + (prow * a.s.hq + head) * D;
+#pragma unroll
+      for (int mb = 0; mb < DB; ++mb)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4)
+          *(f32x4*)(op + 32 * mb + 8 * g4 + 4 * hh) =
+              f32x4{oacc[rh][mb][4 * g4] * inv, oacc[rh][mb][4 * g4 + 1] * inv, oacc[rh][mb][4 * g4 + 2] * inv,
+                    oacc[rh][mb][4 * g4 + 3] * inv};
+      if (hh == 0) a.part_lse[prow * a.s.hq + head] = lse;
+    }
   }
 }
 
@@ -343,6 +746,14 @@ __global__ __launch_bounds__(256) void fwd_merge_kernel(FwdArgs a) {
 hipError_t launch_fwd_main(const FwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_items);
   if (bf16) {
+    const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
+    if (a.s.rw % 2 == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
+        a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 4 waves of 64 rows
+      const dim3 block(4 * 64);
+      if (a.s.d == 128) hipLaunchKernelGGL((fwd_bf16_w64_kernel<128, 4, PSATTN_FWD_NS>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((fwd_bf16_w64_kernel<64, 4, PSATTN_FWD_NS>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
     const dim3 block(a.s.nw * 64);
     if (a.s.d == 128) {
       PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<128, W_, 2>), grid, block, 0, st, a));

@@ -649,6 +649,7 @@ psattn_status psattn_fwd(const psattn_tree* t, const void* Q, const void* K, con
   a.LSE = LSE;
   a.part_o = w.total ? (float*)((uint8_t*)ws + w.o_part_o) : nullptr;
   a.part_lse = w.total ? (float*)((uint8_t*)ws + w.o_part_lse) : nullptr;
+  a.pool_slots = t->pool_slots;
   const bool bf16 = t->dtype == PSATTN_BF16;
   psattn_status s = timed(0, st, [&] { return launch_fwd_main(a, bf16, st); });
   if (s == PSATTN_OK && a.n_merge) s = timed(1, st, [&] { return launch_fwd_merge(a, bf16, st); });

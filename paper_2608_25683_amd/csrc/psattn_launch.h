@@ -17,6 +17,7 @@ struct FwdArgs {
   float* LSE;
   float* part_o;    // [partial rows][Hq][d]
   float* part_lse;  // [partial rows][Hq]
+  int64_t pool_slots;  // rows of the K and V pools
 };
 
 struct BwdArgs {
