@@ -16,6 +16,10 @@
 
 #include "psattn_device.h"
 
+#ifndef PSATTN_DQ_PF
+#define PSATTN_DQ_PF 4
+#endif
+
 namespace psattn {
 namespace {
 
@@ -405,6 +409,315 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 }
 
 // ============================================================================================
+// bf16 dQ kernel, 64 rows per wavefront (the structure of the forward 64-row kernel).  One
+// wavefront per SIMD holds Q, dO and the dQ accumulators of 64 rows of one head in AGPRs and the
+// scores in VGPRs.  Stage j issues the S = K Q^T and dP = V dO^T MFMAs of 32-key block j+1 and
+// the dQ^T += K^T dS^T MFMAs of block j-1, and between them computes P = exp2(S c - LSE log2 e)
+// and dS = P (dP - Delta) of block j.  Every K or V fragment read from LDS feeds two MFMAs.
+template <int D, int NW, int NS>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1))) void bwd_dq_bf16_w64_kernel(BwdArgs a) {
+  constexpr int RB = D * 2;
+  constexpr int CPR = D / 8;
+  constexpr int RPI = 64 / CPR;
+  constexpr int TB = KV_TILE * RB;
+  constexpr int NI = KV_TILE / RPI;
+  constexpr int IPW = NI / NW;
+  constexpr int KS = D / 16;                     // S (and dP) MFMAs per row half and block
+  constexpr int DB = D / 32;
+  constexpr int NDQ = 2 * DB;                    // dQ MFMAs per row half and block
+  constexpr int TPB = IDX_BLK / KV_TILE;
+  constexpr int CPW = 2 * IPW;
+  static_assert(NI % NW == 0 && (NS == 3 || NS == 4) && NS - 1 <= TPB, "tile copy split / ring depth");
+  static_assert(D == 128 || D == 64, "head_dim");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];
+  __shared__ int s_slot[2][IDX_BLK];
+
+  const FwdItem it = a.plan.fwd[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int rw2 = a.s.rw >> 1;
+  const int head = it.head0 + wave / rw2;
+  const int hk = it.head0 / a.s.g;
+  const int nkv = it.nkv;
+  const int* kvl = a.plan.kv_list + it.kv_off;
+  const int ntiles = (nkv + KV_TILE - 1) / KV_TILE;
+
+  for (int i = tid; i < IDX_BLK; i += NW * 64) {
+    s_slot[0][i] = kvl[min(i, nkv - 1)];
+    if (nkv > IDX_BLK) s_slot[1][i] = kvl[min(IDX_BLK + i, nkv - 1)];
+  }
+
+  int ridx[2], row[2], lim[2];
+  bool row_ok[2];
+  float lse2[2], del[2];
+  bf16x8 qreg[2][KS], doreg[2][KS];
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh) {
+    ridx[rh] = (wave % rw2) * 64 + 32 * rh + l32;
+    row_ok[rh] = ridx[rh] < it.nq;
+    row[rh] = a.plan.q_list[it.q_off + (row_ok[rh] ? ridx[rh] : it.nq - 1)];
+    lim[rh] = min(nkv - 1, a.plan.row_pos[row[rh]] - it.kv_pos0);
+    lse2[rh] = a.lse2[(size_t)head * a.s.ns + row[rh]];
+    del[rh] = a.delta[(size_t)head * a.s.ns + row[rh]];
+    const size_t o = ((size_t)row[rh] * a.s.hq + head) * D + 8 * hh;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      qreg[rh][s] = as_bf(ld16((const bf16_t*)a.Q + o + 16 * s));
+      doreg[rh][s] = as_bf(ld16((const bf16_t*)a.dO + o + 16 * s));
+    }
+  }
+
+  const int koff0 = tile_off<D>(l32, hh);                  // K/V rows l32, chunk 2s + hh: koff0 ^ (s << 5)
+  int toff[2];                                             // K^T reads, d block mb: toff ^ (mb << 6)
+  {
+    const int r4 = (lane & 15) >> 2, j = lane & 3, dsub = 16 * ((lane >> 4) & 1);
+#pragma unroll
+    for (int rd = 0; rd < 2; ++rd) toff[rd] = tile_off<D>(8 * rd + 4 * hh + r4, (dsub + 4 * j) >> 3) + 8 * (j & 1);
+  }
+
+  const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
+  const uint8_t* Kb = (const uint8_t*)a.K + (size_t)hk * D * sizeof(bf16_t);
+  const uint8_t* Vb = (const uint8_t*)a.V + (size_t)hk * D * sizeof(bf16_t);
+  const int crow = lane / CPR, cpc = lane % CPR;
+  const uint32_t smem_base = lds_addr(&smem[0][0][0]);
+  auto issue_slots = [&](int t, int (&slot)[IPW]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int key = min(t * KV_TILE + (wave + NW * i) * RPI + crow, nkv - 1);
+      slot[i] = s_slot[(key / IDX_BLK) & 1][key % IDX_BLK];
+    }
+  };
+  auto issue_copy1 = [&](int rs, int i, int slot, int tensor) __attribute__((always_inline)) {
+    const int k = wave + NW * i;
+    const int r = k * RPI + crow;
+    const uint32_t dst = smem_base + (uint32_t)((rs * 2 + tensor) * TB) + k * 1024;
+    const uint32_t off = __umul24((uint32_t)slot, kv_stride) + ((cpc ^ swz<D>(r)) << 4);
+    copy16_to_lds_off(tensor ? Vb : Kb, off, dst);
+  };
+  // all copies into ring slot t % NS, of tile min(t, ntiles - 1) (see the forward kernel)
+  auto issue = [&](int t) __attribute__((always_inline)) {
+    int slot[IPW];
+    issue_slots(min(t, ntiles - 1), slot);
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      issue_copy1(t % NS, i, slot[i], 0);
+      issue_copy1(t % NS, i, slot[i], 1);
+    }
+  };
+  auto fetch_index_block = [&](int b) __attribute__((always_inline)) {
+    if (b * IDX_BLK >= nkv) return;
+    for (int w = wave; w < IDX_BLK / 64; w += NW)
+      copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
+  };
+
+  f32x16 dq[2][DB];
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+    for (int mb = 0; mb < DB; ++mb) {
+      dq[rh][mb] = f32x16{};
+      pin_a(dq[rh][mb]);
+    }
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      pin_a(qreg[rh][s]);
+      pin_a(doreg[rh][s]);
+    }
+  valu_fence();
+  const float c = a.s.scale * kLog2e;
+
+  auto mask_elem = [&](f32x16 (&S)[2], int rh, int v, int kb) __attribute__((always_inline)) {
+    const int x = lim[rh] - kb - 4 * hh;    // element v holds key kb + 4*hh + 8*(v/4) + v%4
+    S[rh][v] = (8 * (v >> 2) + (v & 3) > x) ? kNegInf : S[rh][v];
+  };
+  // ---- one stage.  Sc, dPc: block j (dS now); Sn, dPn: block j+1 (MFMAs now, K and V rows at
+  // Kn, Vn); dSp: dS of block j-1 (dQ MFMAs now, K rows at Kp); dSc: block j's dS (written).
+  auto stage = [&](f32x16 (&Sc)[2], f32x16 (&dPc)[2], f32x16 (&Sn)[2], f32x16 (&dPn)[2],
+                   const bf16x8 (&dSp)[2][2], bf16x8 (&dSc)[2][2], const uint8_t* Kn, const uint8_t* Vn,
+                   const uint8_t* Kp, int kb, auto masked, auto extra, auto dq_first) __attribute__((always_inline)) {
+    // element e = 16 rh + v: scaled and shifted at chunk F(e), exponentiated at F(e)+1,
+    // multiplied by dP - Delta at F(e)+2; each 8-element group is packed after its last product
+    auto F = [](int e) constexpr { return (e * 29) / 32; };
+    auto chunk = [&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      static_for<32>([&](auto ec) __attribute__((always_inline)) {
+        constexpr int e = decltype(ec)::value, rh = e / 16, v = e % 16;
+        if constexpr (F(e) == q) {
+          if constexpr (decltype(masked)::value) mask_elem(Sc, rh, v, kb);
+          Sc[rh][v] = fmaf(Sc[rh][v], c, -lse2[rh]);
+          dPc[rh][v] = dPc[rh][v] - del[rh];
+        }
+        if constexpr (F(e) + 1 == q) Sc[rh][v] = fast_exp2(Sc[rh][v]);
+        if constexpr (F(e) + 2 == q) dPc[rh][v] = Sc[rh][v] * dPc[rh][v];
+        if constexpr (v % 8 == 7 && F(e) + 2 == q) {
+          dSc[rh][v / 8] = pack8(dPc[rh], 8 * (v / 8));
+          anchor(dSc[rh][v / 8]);
+        }
+      });
+    };
+    static_assert(F(31) + 2 <= 31, "dS schedule");
+    bf16x8 kf[KS], vf[KS], tf[NDQ];
+    auto load_k = [&](int s) __attribute__((always_inline)) {
+      kf[s] = as_bf(ld16(Kn + (koff0 ^ (s << 5))));
+      vf[s] = as_bf(ld16(Vn + (koff0 ^ (s << 5))));
+    };
+    auto load_t = [&](int u) __attribute__((always_inline)) {   // u = DB * t2 + mb
+      const int t2 = u / DB, mb = u % DB;
+      const uint8_t* kp = Kp + 16 * t2 * RB;
+      tf[u] = as_bf(lds_tr(kp + (toff[0] ^ (mb << 6))), lds_tr(kp + (toff[1] ^ (mb << 6))));
+    };
+    // fragments in use order: (K, V) pairs of the S and dP MFMAs and K^T fragments of the dQ
+    // MFMAs, in the order the stage issues them; each is read PF pairs ahead
+    constexpr bool DQF = decltype(dq_first)::value;
+    constexpr int PF = PSATTN_DQ_PF;
+    auto load_frag = [&](int f) __attribute__((always_inline)) {
+      if (DQF) {
+        if (f < NDQ) load_t(f);
+        else if (f < NDQ + KS) load_k(f - NDQ);
+      } else {
+        if (f < KS) load_k(f);
+        else if (f < KS + NDQ) load_t(f - KS);
+      }
+    };
+#pragma unroll
+    for (int f = 0; f < PF; ++f) load_frag(f);
+    constexpr int NS_SLOTS = 4 * KS, NQ_SLOTS = 2 * NDQ, NSLOT = NS_SLOTS + NQ_SLOTS;
+    auto slot = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      constexpr int is = DQF ? (i >= NQ_SLOTS ? i - NQ_SLOTS : -1) : (i < NS_SLOTS ? i : -1);   // S/dP slot
+      constexpr int iq = DQF ? (i < NQ_SLOTS ? i : -1) : (i >= NS_SLOTS ? i - NS_SLOTS : -1);   // dQ slot
+      if constexpr (is >= 0) {
+        constexpr int s = is / 4, w = is % 4, rh = w & 1;
+        if constexpr (w == 0) load_frag((DQF ? NDQ : 0) + s + PF);
+        if constexpr (w < 2) {
+          if constexpr (s == 0) mma_v_first(Sn[rh], kf[s], qreg[rh][s]);
+          else mma_v(Sn[rh], kf[s], qreg[rh][s]);
+        } else {
+          if constexpr (s == 0) mma_v_first(dPn[rh], vf[s], doreg[rh][s]);
+          else mma_v(dPn[rh], vf[s], doreg[rh][s]);
+        }
+      } else {
+        constexpr int u = iq / 2, rh = iq % 2;
+        constexpr int t2 = u / DB, mb = u % DB;
+        if constexpr (rh == 0) load_frag((DQF ? 0 : KS) + u + PF);
+        mma_a(dq[rh][mb], tf[u], dSp[rh][t2]);
+      }
+      static_for<(32 * (i + 1)) / NSLOT - (32 * i) / NSLOT>([&](auto dq_) __attribute__((always_inline)) {
+        chunk(IntC<(32 * i) / NSLOT + decltype(dq_)::value>{});
+      });
+      extra(ic);
+      sched_fence();
+    };
+    static_for<NSLOT>(slot);
+  };
+
+  wait_vmem<0>();
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p) issue(p);
+  wait_vmem<CPW * (NS - 2)>();
+  __syncthreads();
+
+  f32x16 SA[2], SB[2], dPA[2], dPB[2];
+  bf16x8 dSA[2][2], dSB[2][2];
+  // block 0's S and dP; block -1's dS is zero (its dQ products, on tile 0's K rows, add nothing)
+  {
+    const uint8_t* K0 = &smem[0][0][0];
+    const uint8_t* V0 = &smem[0][1][0];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const bf16x8 k = as_bf(ld16(K0 + (koff0 ^ (s << 5))));
+      const bf16x8 v = as_bf(ld16(V0 + (koff0 ^ (s << 5))));
+#pragma unroll
+      for (int rh = 0; rh < 2; ++rh) {
+        if (s == 0) {
+          mma_v_first(SA[rh], k, qreg[rh][s]);
+          mma_v_first(dPA[rh], v, doreg[rh][s]);
+        } else {
+          mma_v(SA[rh], k, qreg[rh][s]);
+          mma_v(dPA[rh], v, doreg[rh][s]);
+        }
+      }
+    }
+#pragma unroll
+    for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) dSB[rh][t2] = bf16x8{};
+    mfma_fence();
+  }
+
+  // Tile t+NS-1 is copied during tile t: its V rows in stage 2t (V of tile t-1 was last read by
+  // the dP products of block 2t-1, before the previous barrier), its K rows in stage 2t+1
+  // (after the barrier that ends the dQ products of block 2t-1 on K of tile t-1).
+  auto tile = [&](int t, auto masked) __attribute__((always_inline)) {
+    const uint8_t* Kt = &smem[t % NS][0][0];
+    const uint8_t* Vt = &smem[t % NS][1][0];
+    const uint8_t* Kprev = t > 0 ? &smem[(t + NS - 1) % NS][0][0] + 32 * RB : Kt;
+    const int tn = t + NS - 1;
+    int slot[IPW];
+    issue_slots(min(tn, ntiles - 1), slot);
+    auto vcopies = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (i % 6 == 3 && i / 6 < IPW) issue_copy1(tn % NS, i / 6, slot[i / 6], 1);
+    };
+    // stage 2t: S, dP of block 2t+1, dQ of block 2t-1, dS of block 2t; V copies
+    stage(SA, dPA, SB, dPB, dSB, dSA, Kt + 32 * RB, Vt + 32 * RB, Kprev, t * KV_TILE, masked, vcopies, Flag<false>{});
+    wait_vmem<(2 * NS - 5) * IPW>();
+    __syncthreads();
+    auto kcopies = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (i % 6 == 3 && i / 6 < IPW) issue_copy1(tn % NS, i / 6, slot[i / 6], 0);
+      if constexpr (i == 6 * IPW + 3) {
+        if (tn < ntiles && tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
+      }
+    };
+    // stage 2t+1: dQ of block 2t first (K rows resident before the barrier), then S, dP of block
+    // 2t+2 (tile t+1; unused past the last tile), dS of block 2t+1; K copies
+    stage(SB, dPB, SA, dPA, dSA, dSB, &smem[(t + 1) % NS][0][0], &smem[(t + 1) % NS][1][0], Kt,
+          t * KV_TILE + 32, masked, kcopies, Flag<true>{});
+  };
+  int t = 0;
+  for (; t < min(it.nfull, ntiles); ++t) tile(t, Flag<false>{});
+  for (; t < ntiles; ++t) tile(t, Flag<true>{});
+  wait_vmem<0>();   // no copy may still be writing this workgroup's LDS when it ends
+  // dQ of the last block
+  {
+    const uint8_t* Kl = &smem[(ntiles - 1) % NS][0][0] + 32 * RB;
+#pragma unroll
+    for (int u = 0; u < NDQ; ++u) {
+      const int t2 = u / DB, mb = u % DB;
+      const uint8_t* kp = Kl + 16 * t2 * RB;
+      const bf16x8 k = as_bf(lds_tr(kp + (toff[0] ^ (mb << 6))), lds_tr(kp + (toff[1] ^ (mb << 6))));
+      mma_a(dq[0][mb], k, dSB[0][t2]);
+      mma_a(dq[1][mb], k, dSB[1][t2]);
+    }
+    mfma_fence();
+#pragma unroll
+    for (int rh = 0; rh < 2; ++rh)
+#pragma unroll
+      for (int mb = 0; mb < DB; ++mb) pin_a(dq[rh][mb]);
+  }
+
+  const float scale = a.s.scale;
+#pragma unroll
+  for (int rh = 0; rh < 2; ++rh) {
+    if (!row_ok[rh]) continue;
+    float* dst = it.part < 0 ? a.dQ + ((size_t)row[rh] * a.s.hq + head) * D
+                             : a.part_dq + (((size_t)it.part + ridx[rh]) * a.s.hq + head) * D;
+#pragma unroll
+    for (int mb = 0; mb < DB; ++mb)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *(f32x4*)(dst + 32 * mb + 8 * g4 + 4 * hh) =
+            f32x4{dq[rh][mb][4 * g4] * scale, dq[rh][mb][4 * g4 + 1] * scale, dq[rh][mb][4 * g4 + 2] * scale,
+                  dq[rh][mb][4 * g4 + 3] * scale};
+  }
+}
+
+// ============================================================================================
 // fp32 path (VALU).
 
 template <int D>
@@ -675,6 +988,14 @@ hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st) {
 hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_fwd);
   if (bf16) {
+    const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
+    if (a.s.rw % 2 == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
+        a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 4 waves of 64 rows
+      const dim3 block(4 * 64);
+      if (a.s.d == 128) hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<128, 4, 4>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<64, 4, 4>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
     const dim3 block(a.s.nw * 64);
     if (a.s.d == 128) {
       PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<128, W_, 2>), grid, block, 0, st, a));

@@ -693,6 +693,7 @@ psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, con
   a.part_dq = (float*)(wb + w.o_part_dq);
   a.part_dk = (float*)(wb + w.o_part_dk);
   a.part_dv = (float*)(wb + w.o_part_dv);
+  a.pool_slots = t->pool_slots;
   const bool bf16 = t->dtype == PSATTN_BF16;
   psattn_status s = timed(2, st, [&] { return launch_bwd_pre(a, bf16, st); });
   if (s == PSATTN_OK) s = timed(3, st, [&] { return launch_bwd_kv(a, bf16, st); });

@@ -38,6 +38,7 @@ struct BwdArgs {
   float* part_dq;  // [partial rows][Hq][d]
   float* part_dk;  // [partial tiles][BKV_TILE][d]; each tile belongs to one kv head
   float* part_dv;
+  int64_t pool_slots;  // rows of the K and V pools
 };
 
 // Each launcher enqueues one kernel on stream and returns the launch status.
