@@ -409,6 +409,418 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 }
 
 // ============================================================================================
+// bf16 dK/dV kernel, one wavefront per SIMD.  Four wavefronts: wave w owns keys 32w .. 32w+31
+// of the tile for every query head; its K and V rows (the B operands of S = Q K^T and
+// dP = dO V^T) and its dK and dV accumulators stay in AGPRs for the whole item.  The consumer
+// rows stream through LDS one step at a time (a step is a 32-row subtile of one query head:
+// Q, dO and their LSE log2 e and Delta), in a five-deep ring.  Iteration i issues the dV/dK
+// MFMAs of step i-1 (dV += P^T dO, dK += dS^T Q), then the S and dP MFMAs of step i+1, and
+// between them computes P = exp2(S c - LSE log2 e) and dS = P (dP - Delta) of step i.
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void bwd_kv_bf16_1w_kernel(BwdArgs a) {
+  constexpr int RB = D * 2;
+  constexpr int LRB = D == 128 ? 8 : 7;       // log2(RB)
+  constexpr int CPR = D / 8;
+  constexpr int RPI = 64 / CPR;
+  constexpr int QB = Q_SUB * RB;              // bytes per Q or dO subtile of one head
+  constexpr int NI = Q_SUB / RPI;             // copy instructions per subtile and tensor
+  constexpr int KS = D / 16, DB = D / 32;
+  constexpr int SPB = IDX_BLK / Q_SUB;        // subtiles per staged row block
+  constexpr int NR = 5;                       // step ring: steps i-1 .. i+3
+  constexpr int CPS = 2 * NI / 4;             // copies every wave issues per step (Q and dO)
+  static_assert((2 * NI) % 4 == 0 && (1 << LRB) == RB, "copy split");
+  static_assert(SPB > NR + 2, "the first NR steps read row block 0; a buffer is refilled after its readers");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NR][2][QB];   // [step slot][Q | dO]
+  __shared__ __attribute__((aligned(16))) float s_stat[NR][2][Q_SUB];  // [step slot][LSE*log2e | Delta]
+  __shared__ int s_row[2][IDX_BLK];
+  __shared__ int s_qpos[2][IDX_BLK];
+  const uint32_t smem_base = lds_addr(&smem[0][0][0]), stat_base = lds_addr(&s_stat[0][0][0]);
+
+  const BkvItem it = a.plan.bkv[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int hk = it.hk, G = a.s.g, hq = a.s.hq, ns = a.s.ns;
+  const int nq = it.nq;
+  const int* ql = a.plan.q_list + it.q_off;
+  const int crow = lane / CPR, cpc = lane % CPR;
+  const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
+
+  {
+    const int r = ql[min(tid, nq - 1)];
+    s_row[0][tid] = r;
+    s_qpos[0][tid] = tid < nq ? a.plan.row_pos[r] : -1;
+  }
+  int pre_row = 0, pre_qpos = -1;
+  if (nq > IDX_BLK) {
+    pre_row = ql[min(IDX_BLK + tid, nq - 1)];
+    pre_qpos = IDX_BLK + tid < nq ? a.plan.row_pos[pre_row] : -1;
+  }
+  // K and V rows of this wave's keys: B operands (lane <-> key, 8 consecutive head_dim entries
+  // per k-slot)
+  bf16x8 kreg[KS], vreg[KS];
+  {
+    const int key = min(32 * wave + l32, it.nk - 1);
+    const size_t o = (size_t)__umul24((uint32_t)a.plan.kv_list[it.kv_off + key], kv_stride) +
+                     (size_t)hk * D * sizeof(bf16_t) + 16 * hh;
+    const uint8_t* kp = (const uint8_t*)a.K + o;
+    const uint8_t* vp = (const uint8_t*)a.V + o;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      kreg[s] = as_bf(ld16(kp + 32 * s));
+      vreg[s] = as_bf(ld16(vp + 32 * s));
+    }
+  }
+  const int kpos = it.kv_pos0 + 32 * wave + l32;
+  f32x16 dk[DB], dv[DB];
+#pragma unroll
+  for (int nb = 0; nb < DB; ++nb) {
+    dk[nb] = f32x16{};
+    dv[nb] = f32x16{};
+    pin_a(dk[nb]);
+    pin_a(dv[nb]);
+  }
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    pin_a(kreg[s]);
+    pin_a(vreg[s]);
+  }
+  valu_fence();
+
+  const int nsub = (nq + Q_SUB - 1) / Q_SUB;
+  const int nsteps = nsub * G;                // step = subtile * G + head
+  // the row indices one step's copies read from the staged block, fetched into registers one
+  // iteration ahead so that no copy waits on an LDS read
+  struct Rows {
+    int r[CPS];   // row of copy instruction i of this wave
+    int st;       // row of the statistics element of this lane
+  };
+  auto fetch_rows = [&](int step) __attribute__((always_inline)) {
+    const int sub = min(step, nsteps - 1) / G;
+    const int* rows = &s_row[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
+    Rows o;
+#pragma unroll
+    for (int i = 0; i < CPS; ++i) o.r[i] = rows[((wave + 4 * i) % NI) * RPI + crow];
+    o.st = rows[l32];
+    return o;
+  };
+  // copy instruction j (< CPS) of step min(step, nsteps-1) into ring slot step % NR, and the
+  // statistics copy (wave 0).  Past the last step a copy refills a slot no one reads, so every
+  // step issues the same copies and waits the same.
+  auto issue_one = [&](int step, int rs, const Rows& rw, int j) __attribute__((always_inline)) {
+    const int sc = min(step, nsteps - 1);
+    const int h = sc % G;
+    const int k = wave + 4 * j;              // (tensor, instruction)
+    const int tens = k / NI, ins = k % NI;
+    const int r = ins * RPI + crow;
+    const uint32_t off = ((uint32_t)(rw.r[j] * hq + hk * G + h) << LRB) + ((cpc ^ swz<D>(r)) << 4);
+    copy16_to_lds_off(tens ? a.dO : a.Q, off, smem_base + (uint32_t)((rs * 2 + tens) * QB) + ins * 1024);
+  };
+  auto issue_stat = [&](int step, int rs, const Rows& rw) __attribute__((always_inline)) {
+    if (wave == 0) {   // LSE*log2e (lanes 0-31) and Delta (lanes 32-63) of the step's rows
+      const int sc = min(step, nsteps - 1);
+      const int h = sc % G;
+      const float* src = hh ? a.kv_nd : a.kv_nls;
+      copy4_to_lds_at(src + (size_t)(hk * G + h) * ns + rw.st, stat_base + (uint32_t)rs * (2 * Q_SUB * 4));
+    }
+  };
+
+  const float c = a.s.scale * kLog2e;
+  const int arow = l32 * RB, asw = swz<D>(l32);
+  const int r4 = (lane & 15) >> 2, jq = lane & 3, dsub = 16 * ((lane >> 4) & 1);
+  const int tcol = (dsub + 4 * jq) >> 3, tbyte = 8 * (jq & 1);
+  const int trow0 = (4 * hh + r4) * RB, tsw0 = swz<D>(4 * hh + r4);
+  const int trow1 = (8 + 4 * hh + r4) * RB, tsw1 = swz<D>(8 + 4 * hh + r4);
+  // this lane's byte offsets, within a Q or dO subtile, of its fragment reads: computed once, so
+  // that a read address is one add of the (uniform) subtile offset
+  uint32_t aoff[KS], toff0[DB], toff1[DB];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) aoff[s] = arow + (((2 * s + hh) ^ asw) << 4);
+#pragma unroll
+  for (int nb = 0; nb < DB; ++nb) {
+    toff0[nb] = trow0 + (((4 * nb + tcol) ^ tsw0) << 4) + tbyte;
+    toff1[nb] = trow1 + (((4 * nb + tcol) ^ tsw1) << 4) + tbyte;
+  }
+  const uint8_t* const sm = &smem[0][0][0];
+  // base: byte offset of a subtile in smem
+  auto ld_a = [&](uint32_t base, int s) __attribute__((always_inline)) { return as_bf(ld16(sm + (base + aoff[s]))); };
+  auto ld_t = [&](uint32_t base, int u) __attribute__((always_inline)) {   // u = DB * t2 + nb
+    const int t2 = u / DB, nb = u % DB;
+    const uint32_t b = base + 16 * t2 * RB;
+    return as_bf(lds_tr(sm + (b + toff0[nb])), lds_tr(sm + (b + toff1[nb])));
+  };
+
+  // ---- iteration i, NSLOT MFMA slots (a pair of slots per fragment):
+  //   pairs 0 .. NT-1: dV[nb] += P^T dO and dK[nb] += dS^T Q of step i-1 (pair u = DB*t2 + nb)
+  //   then:            S = Q K^T and dP = dO V^T of step i+1 (pair = k-step s)
+  // with P and dS of step i computed between them.  Sc/dPc: step i; Sn/dPn: step i+1 (written);
+  // Pp/Sp: packed P and dS of step i-1; Pc/Sc2: of step i (written).
+  // Fragments are read PF pairs ahead of their MFMAs; the last pairs read the first PF dV/dK
+  // fragments of iteration i+1 (step i's rows, long landed), so an iteration never starts with
+  // an empty queue.  After slot BAR (MFMAs in flight) the wave waits for its copies of step i+1,
+  // then a barrier: every wave is past iteration i-1, so step i+1 is in LDS and step i-2's ring
+  // slot is free.  The copies of step i+3 into it follow, three slots apart, then (at a subtile
+  // boundary) the row indices of step i+4.  A row block is staged in the iteration that fetches
+  // the rows of its first step; the buffer it overwrites last held the block before the previous
+  // one, whose readers (at least SPB*G >= 8 steps earlier) are all past the last barrier.
+  // The S and dP accumulators of step i+1 are loaded with -LSE/scale and -Delta of its rows right
+  // after the barrier (and -inf where the causal mask hides a pair), so that the MFMAs leave
+  // S - LSE/scale and dP - Delta: P = exp2(c S') and dS = P dP' take two VALU products.
+  constexpr int NT = 2 * DB;                  // dV/dK slot pairs
+  constexpr int PF = 3;
+  constexpr int NSLOT = 2 * NT + 2 * KS;
+  constexpr int BAR = 2 * (NT - PF) - 1 < 3 ? 2 * (NT - PF) - 1 : 3;
+  constexpr int CP0 = BAR + 1, CPD = 3;       // copy j of step i+3 at slot CP0 + CPD*j
+  constexpr int ST_SLOT = CP0 + CPD * CPS, ROW_SLOT = ST_SLOT + 2;
+  constexpr int INIT_SLOT = BAR + 1, MASK_SLOT = 2 * NT - 3;
+  static_assert(BAR >= 1 && ROW_SLOT < NSLOT && INIT_SLOT + 1 < MASK_SLOT, "iteration schedule");
+  bf16x8 ftv[NT], ftk[NT];                    // transposed dO and Q fragments of the dV/dK pairs
+  Rows rows_nx;                               // rows of the next step to copy
+  // element v of a step's S and dP (row 8*(v/4) + 4*hh + v%4) starts at -LSE/scale and -Delta
+  auto init_acc = [&](f32x16& S, f32x16& dP, int slot, auto part) __attribute__((always_inline)) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 x = *(const f32x4*)&s_stat[slot][decltype(part)::value][8 * g + 4 * hh];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if constexpr (decltype(part)::value == 0) S[4 * g + k] = x[k];
+        else dP[4 * g + k] = x[k];
+      }
+    }
+  };
+  // the causal mask, on a step whose rows may see only part of the tile (or lie past the list,
+  // position -1): a hidden (row, key) pair's S starts at -inf.  Every other step skips it.
+  auto mask_acc = [&](f32x16& S, int step) __attribute__((always_inline)) {
+    const int sub = step / G, r0 = sub * Q_SUB;
+    if (step < nsteps && ((r0 + Q_SUB > it.mask_lo && r0 < it.mask_hi) || r0 + Q_SUB > nq)) {
+      const int* qpp = &s_qpos[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int4 q = *(const int4*)&qpp[8 * g + 4 * hh];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) S[4 * g + k] = kpos > q[k] ? kNegInf : S[4 * g + k];
+      }
+    }
+  };
+  auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
+                  bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i, const int (&ring)[NR]) __attribute__((always_inline)) {
+    const int sn3 = i + NR - 2, sn4 = sn3 + 1;
+    const int sub4 = sn4 / G;
+    const bool new_blk = sn4 < nsteps && sn4 % G == 0 && sub4 % SPB == 0;
+    // ring[k]: slot of step i-1+k (rotated, not derived from i, so that a read address stays one
+    // add of a uniform offset); step -1 reads step 0's rows with zero P and dS, never an
+    // unwritten slot
+    const int rp = i > 0 ? ring[0] : ring[1], rc = ring[1], rn = ring[2], rs3 = ring[NR - 1];
+    const uint32_t Qp = rp * 2 * QB, dOp = Qp + QB;
+    const uint32_t Qc = rc * 2 * QB, dOc = Qc + QB;
+    const uint32_t Qn = rn * 2 * QB, dOn = Qn + QB;
+    if (new_blk) {
+      const int blk = sub4 / SPB;
+      s_row[blk & 1][tid] = pre_row;
+      s_qpos[blk & 1][tid] = pre_qpos;
+    }
+    bf16x8 fq[KS], fo[KS];
+    auto load_frag = [&](int f) __attribute__((always_inline)) {
+      if (f < NT) {
+        ftv[f] = ld_t(dOp, f);
+        ftk[f] = ld_t(Qp, f);
+      } else if (f < NT + KS) {
+        fq[f - NT] = ld_a(Qn, f - NT);
+        fo[f - NT] = ld_a(dOn, f - NT);
+      } else if (f < NT + KS + PF) {
+        ftv[f - NT - KS] = ld_t(dOc, f - NT - KS);
+        ftk[f - NT - KS] = ld_t(Qc, f - NT - KS);
+      }
+    };
+    // element v of this step's 16 per lane: scaled at F(v), exponentiated at F(v)+1, dS at
+    // F(v)+2; each 8-element half packed after its last one
+    constexpr auto F = [](int v) { return 2 + (v * (NSLOT - 8)) / 16; };
+    static_assert(F(15) + 3 < NSLOT, "P and dS packed within the iteration");
+    auto chunk = [&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      static_for<16>([&](auto vc) __attribute__((always_inline)) {
+        constexpr int v = decltype(vc)::value;
+        if constexpr (F(v) == q) Sc[v] = Sc[v] * c;
+        if constexpr (F(v) + 1 == q) Sc[v] = fast_exp2(Sc[v]);
+        if constexpr (F(v) + 2 == q) dPc[v] = Sc[v] * dPc[v];
+        if constexpr (v % 8 == 7 && F(v) + 3 == q) {
+          Pc[v / 8] = pack8(Sc, 8 * (v / 8));
+          Sc2[v / 8] = pack8(dPc, 8 * (v / 8));
+          anchor(Pc[v / 8]);
+          anchor(Sc2[v / 8]);
+        }
+      });
+    };
+    auto slot = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int si = decltype(ic)::value;
+      constexpr int m = si / 2, w = si % 2;
+      if constexpr (w == 0) load_frag(m + PF);
+      if constexpr (si < 2 * NT) {
+        constexpr int t2 = m / DB, nb = m % DB;
+        if constexpr (w == 0) mma_a(dv[nb], Pp[t2], ftv[m]);
+        else mma_a(dk[nb], Sp[t2], ftk[m]);
+      } else {
+        constexpr int s = m - NT;
+        if constexpr (w == 0) mma_v(Sn, fq[s], kreg[s]);
+        else mma_v(dPn, fo[s], vreg[s]);
+      }
+      chunk(ic);
+      if constexpr (si == BAR) {
+        if (wave == 0) wait_vmem<CPS + 1>();
+        else wait_vmem<CPS>();
+        if (new_blk) wait_lds<0>();   // the staged row block is written before the barrier
+        barrier_only();
+      }
+      if constexpr (si == INIT_SLOT) init_acc(Sn, dPn, rn, IntC<0>{});
+      if constexpr (si == INIT_SLOT + 1) init_acc(Sn, dPn, rn, IntC<1>{});
+      if constexpr (si == MASK_SLOT) mask_acc(Sn, i + 1);
+      if constexpr (si >= CP0 && si < CP0 + CPD * CPS && (si - CP0) % CPD == 0) issue_one(sn3, rs3, rows_nx, (si - CP0) / CPD);
+      if constexpr (si == ST_SLOT) issue_stat(sn3, rs3, rows_nx);
+      if constexpr (si == ROW_SLOT) {
+        if (sn4 % G == 0) rows_nx = fetch_rows(sn4);   // the rows change only with the subtile
+        if (new_blk) {
+          const int nxt = (sub4 / SPB + 1) * IDX_BLK + tid;
+          if (nxt - tid < nq) {
+            pre_row = ql[min(nxt, nq - 1)];
+            pre_qpos = nxt < nq ? a.plan.row_pos[pre_row] : -1;
+          }
+        }
+      }
+      sched_fence();
+    };
+    static_for<NSLOT>(slot);
+  };
+
+  wait_vmem<0>();   // K and V registers, index block
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < NR - 2; ++p) {
+    const Rows rw = fetch_rows(p);
+#pragma unroll
+    for (int j = 0; j < CPS; ++j) issue_one(p, p, rw, j);
+    issue_stat(p, p, rw);
+  }
+  rows_nx = fetch_rows(NR - 2);
+  if (wave == 0) wait_vmem<(NR - 3) * (CPS + 1)>();
+  else wait_vmem<(NR - 3) * CPS>();
+  __syncthreads();
+
+  f32x16 SA, SB, dPA, dPB;
+  bf16x8 PA[2], PB[2], DSA[2], DSB[2];
+  // S and dP of step 0; the P and dS of step -1 are zero (its dV/dK products, on step 0's rows,
+  // add nothing); the first dV/dK fragments of iteration 0 (step 0's rows)
+  {
+    const uint32_t Q0 = 0, dO0 = QB;
+    init_acc(SA, dPA, 0, IntC<0>{});
+    init_acc(SA, dPA, 0, IntC<1>{});
+    mask_acc(SA, 0);
+    valu_fence();
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      mma_v(SA, ld_a(Q0, s), kreg[s]);
+      mma_v(dPA, ld_a(dO0, s), vreg[s]);
+    }
+#pragma unroll
+    for (int f = 0; f < PF; ++f) {
+      ftv[f] = ld_t(dO0, f);
+      ftk[f] = ld_t(Q0, f);
+    }
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      PB[t2] = DSB[t2] = bf16x8{};
+      anchor(PB[t2]);   // the zeros are written here, before the fence, not next to an MFMA
+      anchor(DSB[t2]);
+    }
+    mfma_fence();
+  }
+
+  static_assert(NR == 5, "ring rotation");
+  int ring[NR] = {NR - 1, 0, 1, 2, 3};
+  auto iteration = [&](int i, auto par) __attribute__((always_inline)) {
+    if constexpr (!decltype(par)::value) body(SA, dPA, SB, dPB, PB, DSB, PA, DSA, i, ring);
+    else body(SB, dPB, SA, dPA, PA, DSA, PB, DSB, i, ring);
+    const int r0 = ring[0];
+#pragma unroll
+    for (int k = 0; k + 1 < NR; ++k) ring[k] = ring[k + 1];
+    ring[NR - 1] = r0;
+  };
+  int i = 0;
+  for (; i + 1 < nsteps; i += 2) {
+    iteration(i, Flag<false>{});
+    iteration(i + 1, Flag<true>{});
+  }
+  if (i < nsteps) iteration(i, Flag<false>{});
+  // the S and dP of step nsteps (never used) are still being written: keep their registers
+  // until the MFMAs are done
+  mfma_fence();
+  pin_v(SA);
+  pin_v(SB);
+  pin_v(dPA);
+  pin_v(dPB);
+  wait_vmem<0>();   // no copy may still be writing this workgroup's LDS when it ends
+  // dV/dK of the last step (its rows are in slot (nsteps-1) % NR)
+  {
+    const bool odd_last = (nsteps - 1) & 1;
+    const int rl = ring[0];   // slot of step nsteps-1
+    const uint32_t Ql = rl * 2 * QB, dOl = Ql + QB;
+    auto last = [&](const bf16x8 (&Pl)[2], const bf16x8 (&Sl)[2]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < NT; ++u) {   // the first PF fragments were read by the last iteration
+        const int t2 = u / DB, nb = u % DB;
+        const bf16x8 tv = u < PF ? ftv[u] : ld_t(dOl, u), tk = u < PF ? ftk[u] : ld_t(Ql, u);
+        mma_a(dv[nb], Pl[t2], tv);
+        mma_a(dk[nb], Sl[t2], tk);
+      }
+    };
+    // one code path: the last step's P and dS are moved into the even buffers first
+    if (odd_last) {
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        PA[t2] = PB[t2];
+        DSA[t2] = DSB[t2];
+      }
+    }
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      anchor(PA[t2]);
+      anchor(DSA[t2]);
+    }
+    valu_fence();
+    last(PA, DSA);
+    mfma_fence();
+#pragma unroll
+    for (int nb = 0; nb < DB; ++nb) {
+      pin_a(dk[nb]);
+      pin_a(dv[nb]);
+    }
+  }
+
+  // accumulator layout: lane <-> head_dim column 32*nb + l32, element v <-> key of the wave
+  const float scale = a.s.scale;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int key = 32 * wave + 8 * (v >> 2) + 4 * hh + (v & 3);
+    if (key >= it.nk) continue;
+    float* kdst;
+    float* vdst;
+    if (it.part < 0) {
+      const size_t o = (size_t)a.plan.kv_list[it.kv_off + key] * a.s.hkv * D + (size_t)hk * D;
+      kdst = a.dK + o;
+      vdst = a.dV + o;
+    } else {
+      const size_t o = ((size_t)it.part * BKV_TILE + key) * D;
+      kdst = a.part_dk + o;
+      vdst = a.part_dv + o;
+    }
+#pragma unroll
+    for (int nb = 0; nb < DB; ++nb) {
+      kdst[32 * nb + l32] = dk[nb][v] * scale;
+      vdst[32 * nb + l32] = dv[nb][v];
+    }
+  }
+}
+
+// ============================================================================================
 // bf16 dQ kernel, 64 rows per wavefront (the structure of the forward 64-row kernel).  One
 // wavefront per SIMD holds Q, dO and the dQ accumulators of 64 rows of one head in AGPRs and the
 // scores in VGPRs.  Stage j issues the S = K Q^T and dP = V dO^T MFMAs of 32-key block j+1 and
@@ -903,6 +1315,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
     const size_t o = (size_t)h * a.s.ns + row;
     a.delta[o] = acc;
     a.lse2[o] = a.LSE[o] * kLog2e;
+    a.kv_nls[o] = -a.LSE[o] / a.s.scale;
+    a.kv_nd[o] = -acc;
   }
 }
 
@@ -976,6 +1390,15 @@ hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st) {
 hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_bkv), block(256);
   if (bf16) {
+    // one wavefront per SIMD: pools and the Q / dO tensors addressed by 32-bit byte offsets
+    const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
+    const int64_t q_bytes = (int64_t)a.s.ns * a.s.hq * a.s.d * 2;
+    if (a.pool_slots <= (1 << 24) && a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX &&
+        q_bytes <= (int64_t)UINT32_MAX && (int64_t)a.s.ns * a.s.hq < (1 << 24)) {
+      if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_1w_kernel<128>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((bwd_kv_bf16_1w_kernel<64>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
     if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_kernel<128>), grid, dim3(512), 0, st, a);
     else hipLaunchKernelGGL((bwd_kv_bf16_kernel<64>), grid, dim3(512), 0, st, a);
   } else {

@@ -116,6 +116,10 @@ __device__ __forceinline__ void copy4_to_lds(const void* g, void* lds_base) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)PSATTN_LDS(void, lds_base));
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
+// copy4_to_lds with the LDS address given directly (wave-uniform)
+__device__ __forceinline__ void copy4_to_lds_at(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
 // Wait until at most N vector-memory loads of this wave are in flight (gfx9 s_waitcnt encoding:
 // vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).  The intrinsic keeps
 // the compiler's own load scoreboard in step, so it inserts no further waits for older loads.
@@ -124,6 +128,16 @@ __device__ __forceinline__ void wait_vmem() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+// Wait until at most N LDS (and scalar memory) operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_lds() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (N << 8));
+}
+// Workgroup barrier without the wait for this wave's outstanding LDS reads that __syncthreads
+// adds; the memory clobber keeps the compiler from moving loads or stores across it.  LDS writes
+// other waves must see after it need a wait_lds<0>() first.
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
 // ---- MFMA through inline assembly, with the register class of each operand chosen here
 // (accumulators and loop-invariant operands in AGPRs, scores in VGPRs).  The compiler does not

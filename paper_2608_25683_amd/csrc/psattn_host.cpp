@@ -495,13 +495,17 @@ FwdWs fwd_ws(const psattn_tree* t) {
   w.total = t->fwd_part_rows ? cur : 0;
   return w;
 }
-struct BwdWs { size_t o_delta, o_lse2, o_part_dq, o_part_dk, o_part_dv, total; };
+struct BwdWs { size_t o_delta, o_lse2, o_kv_nls, o_kv_nd, o_part_dq, o_part_dk, o_part_dv, total; };
 BwdWs bwd_ws(const psattn_tree* t) {
   BwdWs w;
   size_t cur = 0;
   w.o_delta = cur;
   cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
   w.o_lse2 = cur;
+  cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
+  w.o_kv_nls = cur;
+  cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
+  w.o_kv_nd = cur;
   cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
   w.o_part_dq = cur;
   cur = align_up(cur + (size_t)t->fwd_part_rows * t->hq * t->d * 4);
@@ -690,6 +694,8 @@ psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, con
   uint8_t* wb = (uint8_t*)ws;
   a.delta = (float*)(wb + w.o_delta);
   a.lse2 = (float*)(wb + w.o_lse2);
+  a.kv_nls = (float*)(wb + w.o_kv_nls);
+  a.kv_nd = (float*)(wb + w.o_kv_nd);
   a.part_dq = (float*)(wb + w.o_part_dq);
   a.part_dk = (float*)(wb + w.o_part_dk);
   a.part_dv = (float*)(wb + w.o_part_dv);

@@ -35,6 +35,8 @@ struct BwdArgs {
   float* dV;
   float* delta;    // [Hq][Ns]
   float* lse2;     // [Hq][Ns] LSE * log2(e)
+  float* kv_nls;   // [Hq][Ns] -LSE / scale   (start of the dK/dV kernels' S accumulators)
+  float* kv_nd;    // [Hq][Ns] -Delta         (start of their dP accumulators)
   float* part_dq;  // [partial rows][Hq][d]
   float* part_dk;  // [partial tiles][BKV_TILE][d]; each tile belongs to one kv head
   float* part_dv;
