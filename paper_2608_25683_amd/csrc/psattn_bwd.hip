@@ -431,7 +431,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   static_assert((2 * NI) % 4 == 0 && (1 << LRB) == RB, "copy split");
   static_assert(SPB > NR + 2, "the first NR steps read row block 0; a buffer is refilled after its readers");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NR][2][QB];   // [step slot][Q | dO]
-  __shared__ __attribute__((aligned(16))) float s_stat[NR][2][Q_SUB];  // [step slot][LSE*log2e | Delta]
+  __shared__ __attribute__((aligned(16))) float s_stat[NR][2][Q_SUB];  // [step slot][-LSE/scale | -Delta]
   __shared__ int s_row[2][IDX_BLK];
   __shared__ int s_qpos[2][IDX_BLK];
   const uint32_t smem_base = lds_addr(&smem[0][0][0]), stat_base = lds_addr(&s_stat[0][0][0]);
@@ -489,40 +489,43 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
   const int nsub = (nq + Q_SUB - 1) / Q_SUB;
   const int nsteps = nsub * G;                // step = subtile * G + head
-  // the row indices one step's copies read from the staged block, fetched into registers one
-  // iteration ahead so that no copy waits on an LDS read
+  // ---- copies.  Copy instruction j of this wave moves 16 bytes per lane of row r_j = ins*RPI + crow
+  // of a subtile of tensor tens (Q or dO); its source byte offset is the lane's rowoff_j (row of the
+  // list times hq*RB, plus the swizzled column: changes with the subtile) plus hoff = (hk*G + h)*RB
+  // (uniform: changes with the head).  Every wave also copies the step's -LSE/scale (lanes 0-31)
+  // and -Delta (lanes 32-63), the same 256 bytes, so that all waves issue and wait alike.
   struct Rows {
-    int r[CPS];   // row of copy instruction i of this wave
-    int st;       // row of the statistics element of this lane
+    uint32_t off[CPS];   // rowoff_j
+    uint32_t st;         // 4 * row (+ the distance from the -LSE/scale to the -Delta array on lanes 32-63)
   };
-  auto fetch_rows = [&](int step) __attribute__((always_inline)) {
-    const int sub = min(step, nsteps - 1) / G;
+  const uint32_t nd_dist = (uint32_t)((const char*)a.kv_nd - (const char*)a.kv_nls);
+  const uint32_t row_bytes = (uint32_t)hq * RB;
+  auto fetch_rows = [&](int sub) __attribute__((always_inline)) {   // rows of subtile sub (staged)
     const int* rows = &s_row[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
     Rows o;
 #pragma unroll
-    for (int i = 0; i < CPS; ++i) o.r[i] = rows[((wave + 4 * i) % NI) * RPI + crow];
-    o.st = rows[l32];
+    for (int j = 0; j < CPS; ++j) {
+      const int r = ((wave + 4 * j) % NI) * RPI + crow;
+      o.off[j] = (uint32_t)rows[r] * row_bytes + ((cpc ^ swz<D>(r)) << 4);
+    }
+    o.st = (uint32_t)rows[l32] * 4 + (hh ? nd_dist : 0u);
     return o;
   };
-  // copy instruction j (< CPS) of step min(step, nsteps-1) into ring slot step % NR, and the
-  // statistics copy (wave 0).  Past the last step a copy refills a slot no one reads, so every
-  // step issues the same copies and waits the same.
-  auto issue_one = [&](int step, int rs, const Rows& rw, int j) __attribute__((always_inline)) {
-    const int sc = min(step, nsteps - 1);
-    const int h = sc % G;
-    const int k = wave + 4 * j;              // (tensor, instruction)
-    const int tens = k / NI, ins = k % NI;
-    const int r = ins * RPI + crow;
-    const uint32_t off = ((uint32_t)(rw.r[j] * hq + hk * G + h) << LRB) + ((cpc ^ swz<D>(r)) << 4);
-    copy16_to_lds_off(tens ? a.dO : a.Q, off, smem_base + (uint32_t)((rs * 2 + tens) * QB) + ins * 1024);
+  const void* gsrc[CPS];                      // tensor of copy j
+  uint32_t gdst[CPS];                         // its LDS byte offset within a ring slot
+#pragma unroll
+  for (int j = 0; j < CPS; ++j) {
+    const int k = wave + 4 * j, tens = k / NI, ins = k % NI;
+    gsrc[j] = tens ? a.dO : a.Q;
+    gdst[j] = (uint32_t)(tens * QB + ins * 1024);
+  }
+  const uint32_t hoff0 = (uint32_t)(hk * G) * RB, hst0 = (uint32_t)(hk * G) * (uint32_t)ns * 4;
+  // copy j of a step (head h, ring slot byte offset slot_off) into its ring slot
+  auto issue_one = [&](uint32_t slot_off, uint32_t hoff, const Rows& rw, int j) __attribute__((always_inline)) {
+    copy16_to_lds_off(gsrc[j], rw.off[j] + hoff, smem_base + slot_off + gdst[j]);
   };
-  auto issue_stat = [&](int step, int rs, const Rows& rw) __attribute__((always_inline)) {
-    if (wave == 0) {   // LSE*log2e (lanes 0-31) and Delta (lanes 32-63) of the step's rows
-      const int sc = min(step, nsteps - 1);
-      const int h = sc % G;
-      const float* src = hh ? a.kv_nd : a.kv_nls;
-      copy4_to_lds_at(src + (size_t)(hk * G + h) * ns + rw.st, stat_base + (uint32_t)rs * (2 * Q_SUB * 4));
-    }
+  auto issue_stat = [&](uint32_t slot_off, uint32_t hst, const Rows& rw) __attribute__((always_inline)) {
+    copy4_to_lds_off(a.kv_nls, rw.st + hst, stat_base + slot_off / (2 * QB) * (2 * Q_SUB * 4));
   };
 
   const float c = a.s.scale * kLog2e;
@@ -550,6 +553,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     return as_bf(lds_tr(sm + (b + toff0[nb])), lds_tr(sm + (b + toff1[nb])));
   };
 
+  // steps whose rows may see only part of the tile ([mask_lo, mask_hi) of the list) or lie past
+  // the list: [s_lo, s_hi) and [s_pad, nsteps)
+  const int s_lo = it.mask_lo / Q_SUB * G, s_hi = (it.mask_hi + Q_SUB - 1) / Q_SUB * G;
+  const int s_pad = nq / Q_SUB * G;
+  auto is_masked = [&](int step) __attribute__((always_inline)) {
+    return (uint32_t)(step - s_lo) < (uint32_t)(s_hi - s_lo) || (step >= s_pad && step < nsteps);
+  };
+
   // ---- iteration i, NSLOT MFMA slots (a pair of slots per fragment):
   //   pairs 0 .. NT-1: dV[nb] += P^T dO and dK[nb] += dS^T Q of step i-1 (pair u = DB*t2 + nb)
   //   then:            S = Q K^T and dP = dO V^T of step i+1 (pair = k-step s)
@@ -560,12 +571,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // an empty queue.  After slot BAR (MFMAs in flight) the wave waits for its copies of step i+1,
   // then a barrier: every wave is past iteration i-1, so step i+1 is in LDS and step i-2's ring
   // slot is free.  The copies of step i+3 into it follow, three slots apart, then (at a subtile
-  // boundary) the row indices of step i+4.  A row block is staged in the iteration that fetches
-  // the rows of its first step; the buffer it overwrites last held the block before the previous
-  // one, whose readers (at least SPB*G >= 8 steps earlier) are all past the last barrier.
+  // boundary) the row offsets of the next subtile.  A row block is staged in the iteration that
+  // fetches the rows of its first subtile; the buffer it overwrites last held the block before the
+  // previous one, whose readers (at least SPB*G >= 8 steps earlier) are all past the last barrier.
   // The S and dP accumulators of step i+1 are loaded with -LSE/scale and -Delta of its rows right
   // after the barrier (and -inf where the causal mask hides a pair), so that the MFMAs leave
   // S - LSE/scale and dP - Delta: P = exp2(c S') and dS = P dP' take two VALU products.
+  // The loop's bookkeeping is incremental and uniform: the ring of slot offsets rotates, and the
+  // copy step's head, head offsets and subtile advance by one step per iteration (frozen once the
+  // copies pass the last step: they then refill a slot no one reads).
   constexpr int NT = 2 * DB;                  // dV/dK slot pairs
   constexpr int PF = 3;
   constexpr int NSLOT = 2 * NT + 2 * KS;
@@ -575,12 +589,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr int INIT_SLOT = BAR + 1, MASK_SLOT = 2 * NT - 3;
   static_assert(BAR >= 1 && ROW_SLOT < NSLOT && INIT_SLOT + 1 < MASK_SLOT, "iteration schedule");
   bf16x8 ftv[NT], ftk[NT];                    // transposed dO and Q fragments of the dV/dK pairs
-  Rows rows_nx;                               // rows of the next step to copy
+  Rows rows_nx;                               // row offsets of the copy step's subtile
   // element v of a step's S and dP (row 8*(v/4) + 4*hh + v%4) starts at -LSE/scale and -Delta
-  auto init_acc = [&](f32x16& S, f32x16& dP, int slot, auto part) __attribute__((always_inline)) {
+  auto init_acc = [&](f32x16& S, f32x16& dP, uint32_t slot_off, auto part) __attribute__((always_inline)) {
+    const float* st = &s_stat[0][0][0] + slot_off / (2 * QB) * (2 * Q_SUB);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 x = *(const f32x4*)&s_stat[slot][decltype(part)::value][8 * g + 4 * hh];
+      const f32x4 x = *(const f32x4*)&st[decltype(part)::value * Q_SUB + 8 * g + 4 * hh];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         if constexpr (decltype(part)::value == 0) S[4 * g + k] = x[k];
@@ -591,8 +606,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // the causal mask, on a step whose rows may see only part of the tile (or lie past the list,
   // position -1): a hidden (row, key) pair's S starts at -inf.  Every other step skips it.
   auto mask_acc = [&](f32x16& S, int step) __attribute__((always_inline)) {
-    const int sub = step / G, r0 = sub * Q_SUB;
-    if (step < nsteps && ((r0 + Q_SUB > it.mask_lo && r0 < it.mask_hi) || r0 + Q_SUB > nq)) {
+    if (is_masked(step)) {
+      const int sub = step / G;
       const int* qpp = &s_qpos[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -602,20 +617,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     }
   };
+  uint32_t ring[NR];                          // ring[k]: slot byte offset of step i-1+k
+  int h3, subc;                               // head and subtile of the copy step min(i+3, nsteps-1)
+  uint32_t hoff3, hst3;                       // its head offsets in Q/dO rows and in the statistics
   auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
-                  bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i, const int (&ring)[NR]) __attribute__((always_inline)) {
-    const int sn3 = i + NR - 2, sn4 = sn3 + 1;
-    const int sub4 = sn4 / G;
-    const bool new_blk = sn4 < nsteps && sn4 % G == 0 && sub4 % SPB == 0;
-    // ring[k]: slot of step i-1+k (rotated, not derived from i, so that a read address stays one
-    // add of a uniform offset); step -1 reads step 0's rows with zero P and dS, never an
-    // unwritten slot
-    const int rp = i > 0 ? ring[0] : ring[1], rc = ring[1], rn = ring[2], rs3 = ring[NR - 1];
-    const uint32_t Qp = rp * 2 * QB, dOp = Qp + QB;
-    const uint32_t Qc = rc * 2 * QB, dOc = Qc + QB;
-    const uint32_t Qn = rn * 2 * QB, dOn = Qn + QB;
+                  bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i) __attribute__((always_inline)) {
+    // step -1 reads step 0's rows with zero P and dS, never an unwritten slot
+    const uint32_t Qp = i > 0 ? ring[0] : ring[1], dOp = Qp + QB;
+    const uint32_t Qc = ring[1], dOc = Qc + QB;
+    const uint32_t Qn = ring[2], dOn = Qn + QB;
+    const uint32_t slot3 = ring[NR - 1];
+    const bool next_sub = i + NR - 1 < nsteps && h3 == G - 1;   // step i+4 starts a subtile
+    const bool new_blk = next_sub && (subc + 1) % SPB == 0;      // ... and a row block
     if (new_blk) {
-      const int blk = sub4 / SPB;
+      const int blk = (subc + 1) / SPB;
       s_row[blk & 1][tid] = pre_row;
       s_qpos[blk & 1][tid] = pre_qpos;
     }
@@ -640,9 +655,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       constexpr int q = decltype(qc)::value;
       static_for<16>([&](auto vc) __attribute__((always_inline)) {
         constexpr int v = decltype(vc)::value;
-        if constexpr (F(v) == q) Sc[v] = Sc[v] * c;
-        if constexpr (F(v) + 1 == q) Sc[v] = fast_exp2(Sc[v]);
-        if constexpr (F(v) + 2 == q) dPc[v] = Sc[v] * dPc[v];
+        // (each result pinned to its slot: the branches of the iteration would otherwise let the
+        // compiler sink these products to their first use)
+        if constexpr (F(v) == q) {
+          float t = Sc[v] * c;
+          anchor(t);
+          Sc[v] = t;
+        }
+        if constexpr (F(v) + 1 == q) {
+          float t = fast_exp2(Sc[v]);
+          anchor(t);
+          Sc[v] = t;
+        }
+        if constexpr (F(v) + 2 == q) {
+          float t = Sc[v] * dPc[v];
+          anchor(t);
+          dPc[v] = t;
+        }
         if constexpr (v % 8 == 7 && F(v) + 3 == q) {
           Pc[v / 8] = pack8(Sc, 8 * (v / 8));
           Sc2[v / 8] = pack8(dPc, 8 * (v / 8));
@@ -666,20 +695,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
       chunk(ic);
       if constexpr (si == BAR) {
-        if (wave == 0) wait_vmem<CPS + 1>();
-        else wait_vmem<CPS>();
+        wait_vmem<CPS + 1>();
         if (new_blk) wait_lds<0>();   // the staged row block is written before the barrier
         barrier_only();
       }
-      if constexpr (si == INIT_SLOT) init_acc(Sn, dPn, rn, IntC<0>{});
-      if constexpr (si == INIT_SLOT + 1) init_acc(Sn, dPn, rn, IntC<1>{});
+      if constexpr (si == INIT_SLOT) init_acc(Sn, dPn, Qn, IntC<0>{});
+      if constexpr (si == INIT_SLOT + 1) init_acc(Sn, dPn, Qn, IntC<1>{});
       if constexpr (si == MASK_SLOT) mask_acc(Sn, i + 1);
-      if constexpr (si >= CP0 && si < CP0 + CPD * CPS && (si - CP0) % CPD == 0) issue_one(sn3, rs3, rows_nx, (si - CP0) / CPD);
-      if constexpr (si == ST_SLOT) issue_stat(sn3, rs3, rows_nx);
+      if constexpr (si >= CP0 && si < CP0 + CPD * CPS && (si - CP0) % CPD == 0) issue_one(slot3, hoff3, rows_nx, (si - CP0) / CPD);
+      if constexpr (si == ST_SLOT) issue_stat(slot3, hst3, rows_nx);
       if constexpr (si == ROW_SLOT) {
-        if (sn4 % G == 0) rows_nx = fetch_rows(sn4);   // the rows change only with the subtile
+        if (next_sub) {
+          subc += 1;
+          rows_nx = fetch_rows(subc);
+        }
         if (new_blk) {
-          const int nxt = (sub4 / SPB + 1) * IDX_BLK + tid;
+          const int nxt = ((subc / SPB) + 1) * IDX_BLK + tid;
           if (nxt - tid < nq) {
             pre_row = ql[min(nxt, nq - 1)];
             pre_qpos = nxt < nq ? a.plan.row_pos[pre_row] : -1;
@@ -689,20 +720,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       sched_fence();
     };
     static_for<NSLOT>(slot);
+    // the copy step advances to i+4 unless that is past the last step
+    if (i + NR - 1 < nsteps) {
+      const bool wrap = h3 == G - 1;
+      h3 = wrap ? 0 : h3 + 1;
+      hoff3 = wrap ? hoff0 : hoff3 + RB;
+      hst3 = wrap ? hst0 : hst3 + (uint32_t)ns * 4;
+    }
   };
 
   wait_vmem<0>();   // K and V registers, index block
   __syncthreads();
 #pragma unroll
   for (int p = 0; p < NR - 2; ++p) {
-    const Rows rw = fetch_rows(p);
+    const int sc = min(p, nsteps - 1), h = sc % G;
+    const Rows rw = fetch_rows(sc / G);
 #pragma unroll
-    for (int j = 0; j < CPS; ++j) issue_one(p, p, rw, j);
-    issue_stat(p, p, rw);
+    for (int j = 0; j < CPS; ++j) issue_one(p * 2 * QB, hoff0 + h * RB, rw, j);
+    issue_stat(p * 2 * QB, hst0 + (uint32_t)h * ns * 4, rw);
   }
-  rows_nx = fetch_rows(NR - 2);
-  if (wave == 0) wait_vmem<(NR - 3) * (CPS + 1)>();
-  else wait_vmem<(NR - 3) * CPS>();
+  {
+    const int sc = min(NR - 2, nsteps - 1);
+    h3 = sc % G;
+    subc = sc / G;
+    hoff3 = hoff0 + h3 * RB;
+    hst3 = hst0 + (uint32_t)h3 * ns * 4;
+    rows_nx = fetch_rows(subc);
+  }
+  wait_vmem<(NR - 3) * (CPS + 1)>();
   __syncthreads();
 
   f32x16 SA, SB, dPA, dPB;
@@ -735,11 +780,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 
   static_assert(NR == 5, "ring rotation");
-  int ring[NR] = {NR - 1, 0, 1, 2, 3};
+  ring[0] = (NR - 1) * 2 * QB;
+#pragma unroll
+  for (int k = 1; k < NR; ++k) ring[k] = (k - 1) * 2 * QB;
   auto iteration = [&](int i, auto par) __attribute__((always_inline)) {
-    if constexpr (!decltype(par)::value) body(SA, dPA, SB, dPB, PB, DSB, PA, DSA, i, ring);
-    else body(SB, dPB, SA, dPA, PA, DSA, PB, DSB, i, ring);
-    const int r0 = ring[0];
+    if constexpr (!decltype(par)::value) body(SA, dPA, SB, dPB, PB, DSB, PA, DSA, i);
+    else body(SB, dPB, SA, dPA, PA, DSA, PB, DSB, i);
+    const uint32_t r0 = ring[0];
 #pragma unroll
     for (int k = 0; k + 1 < NR; ++k) ring[k] = ring[k + 1];
     ring[NR - 1] = r0;
@@ -761,8 +808,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // dV/dK of the last step (its rows are in slot (nsteps-1) % NR)
   {
     const bool odd_last = (nsteps - 1) & 1;
-    const int rl = ring[0];   // slot of step nsteps-1
-    const uint32_t Ql = rl * 2 * QB, dOl = Ql + QB;
+    const uint32_t Ql = ring[0], dOl = Ql + QB;   // slot of step nsteps-1
     auto last = [&](const bf16x8 (&Pl)[2], const bf16x8 (&Sl)[2]) __attribute__((always_inline)) {
 #pragma unroll
       for (int u = 0; u < NT; ++u) {   // the first PF fragments were read by the last iteration

@@ -120,6 +120,10 @@ __device__ __forceinline__ void copy4_to_lds(const void* g, void* lds_base) {
 __device__ __forceinline__ void copy4_to_lds_at(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
+// 4 bytes per lane from base + off (uniform base, 32-bit per-lane byte offset) to lds + 4 * lane
+__device__ __forceinline__ void copy4_to_lds_off(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
 // Wait until at most N vector-memory loads of this wave are in flight (gfx9 s_waitcnt encoding:
 // vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima).  The intrinsic keeps
 // the compiler's own load scoreboard in step, so it inserts no further waits for older loads.
