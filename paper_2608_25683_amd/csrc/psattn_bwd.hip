@@ -430,6 +430,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr int CPS = 2 * NI / 4;             // copies every wave issues per step (Q and dO)
   static_assert((2 * NI) % 4 == 0 && (1 << LRB) == RB, "copy split");
   static_assert(SPB > NR + 2, "the first NR steps read row block 0; a buffer is refilled after its readers");
+  static_assert(2 * SPB == 16 && IDX_BLK == SPB * Q_SUB, "subtile sub is staged at entry (sub & 15) * Q_SUB");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NR][2][QB];   // [step slot][Q | dO]
   __shared__ __attribute__((aligned(16))) float s_stat[NR][2][Q_SUB];  // [step slot][-LSE/scale | -Delta]
   __shared__ int s_row[2][IDX_BLK];
@@ -501,7 +502,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const uint32_t nd_dist = (uint32_t)((const char*)a.kv_nd - (const char*)a.kv_nls);
   const uint32_t row_bytes = (uint32_t)hq * RB;
   auto fetch_rows = [&](int sub) __attribute__((always_inline)) {   // rows of subtile sub (staged)
-    const int* rows = &s_row[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
+    const int* rows = &s_row[0][0] + (sub & 15) * Q_SUB;
     Rows o;
 #pragma unroll
     for (int j = 0; j < CPS; ++j) {
@@ -605,10 +606,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   };
   // the causal mask, on a step whose rows may see only part of the tile (or lie past the list,
   // position -1): a hidden (row, key) pair's S starts at -inf.  Every other step skips it.
-  auto mask_acc = [&](f32x16& S, int step) __attribute__((always_inline)) {
+  auto mask_acc = [&](f32x16& S, int step, int sub) __attribute__((always_inline)) {   // sub: step's subtile
     if (is_masked(step)) {
-      const int sub = step / G;
-      const int* qpp = &s_qpos[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
+      const int* qpp = &s_qpos[0][0] + (sub & 15) * Q_SUB;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int4 q = *(const int4*)&qpp[8 * g + 4 * hh];
@@ -617,16 +617,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     }
   };
-  uint32_t ring[NR];                          // ring[k]: slot byte offset of step i-1+k
   int h3, subc;                               // head and subtile of the copy step min(i+3, nsteps-1)
+  int h1 = 1 % G, sub1 = 1 / G;               // head and subtile of step i+1
   uint32_t hoff3, hst3;                       // its head offsets in Q/dO rows and in the statistics
   auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
-                  bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i) __attribute__((always_inline)) {
-    // step -1 reads step 0's rows with zero P and dS, never an unwritten slot
-    const uint32_t Qp = i > 0 ? ring[0] : ring[1], dOp = Qp + QB;
-    const uint32_t Qc = ring[1], dOc = Qc + QB;
-    const uint32_t Qn = ring[2], dOn = Qn + QB;
-    const uint32_t slot3 = ring[NR - 1];
+                  bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i, auto pos) __attribute__((always_inline)) {
+    // pos = i mod 2*NR: the ring slots of steps i-1, i, i+1 and i+3 are compile-time constants, so
+    // that a read address is an immediate offset from the lane's base (step -1 reads ring slot
+    // NR-1, zero-filled before the loop, with zero P and dS)
+    constexpr int p = decltype(pos)::value;
+    constexpr uint32_t Qp = (uint32_t)((p + NR - 1) % NR) * 2 * QB, dOp = Qp + QB;
+    constexpr uint32_t Qc = (uint32_t)(p % NR) * 2 * QB, dOc = Qc + QB;
+    constexpr uint32_t Qn = (uint32_t)((p + 1) % NR) * 2 * QB, dOn = Qn + QB;
+    constexpr uint32_t slot3 = (uint32_t)((p + NR - 2) % NR) * 2 * QB;
     const bool next_sub = i + NR - 1 < nsteps && h3 == G - 1;   // step i+4 starts a subtile
     const bool new_blk = next_sub && (subc + 1) % SPB == 0;      // ... and a row block
     if (new_blk) {
@@ -701,7 +704,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
       if constexpr (si == INIT_SLOT) init_acc(Sn, dPn, Qn, IntC<0>{});
       if constexpr (si == INIT_SLOT + 1) init_acc(Sn, dPn, Qn, IntC<1>{});
-      if constexpr (si == MASK_SLOT) mask_acc(Sn, i + 1);
+      if constexpr (si == MASK_SLOT) mask_acc(Sn, i + 1, sub1);
       if constexpr (si >= CP0 && si < CP0 + CPD * CPS && (si - CP0) % CPD == 0) issue_one(slot3, hoff3, rows_nx, (si - CP0) / CPD);
       if constexpr (si == ST_SLOT) issue_stat(slot3, hst3, rows_nx);
       if constexpr (si == ROW_SLOT) {
@@ -720,6 +723,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       sched_fence();
     };
     static_for<NSLOT>(slot);
+    {
+      const bool wrap = h1 == G - 1;
+      h1 = wrap ? 0 : h1 + 1;
+      sub1 += wrap ? 1 : 0;
+    }
     // the copy step advances to i+4 unless that is past the last step
     if (i + NR - 1 < nsteps) {
       const bool wrap = h3 == G - 1;
@@ -729,6 +737,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
   };
 
+  // ring slot NR-1 (read as step -1 by iteration 0) zero-filled
+  for (int k = tid; k < 2 * QB / 16; k += 256) *(u32x4*)&smem[NR - 1][0][16 * k] = u32x4{0, 0, 0, 0};
   wait_vmem<0>();   // K and V registers, index block
   __syncthreads();
 #pragma unroll
@@ -758,7 +768,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const uint32_t Q0 = 0, dO0 = QB;
     init_acc(SA, dPA, 0, IntC<0>{});
     init_acc(SA, dPA, 0, IntC<1>{});
-    mask_acc(SA, 0);
+    mask_acc(SA, 0, 0);
     valu_fence();
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
@@ -779,24 +789,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     mfma_fence();
   }
 
-  static_assert(NR == 5, "ring rotation");
-  ring[0] = (NR - 1) * 2 * QB;
-#pragma unroll
-  for (int k = 1; k < NR; ++k) ring[k] = (k - 1) * 2 * QB;
-  auto iteration = [&](int i, auto par) __attribute__((always_inline)) {
-    if constexpr (!decltype(par)::value) body(SA, dPA, SB, dPB, PB, DSB, PA, DSA, i);
-    else body(SB, dPB, SA, dPA, PA, DSA, PB, DSB, i);
-    const uint32_t r0 = ring[0];
-#pragma unroll
-    for (int k = 0; k + 1 < NR; ++k) ring[k] = ring[k + 1];
-    ring[NR - 1] = r0;
-  };
+  // 2*NR iterations per trip (the S/dP buffers alternate with period 2, the ring with period NR),
+  // leaving after whichever iteration is the last
   int i = 0;
-  for (; i + 1 < nsteps; i += 2) {
-    iteration(i, Flag<false>{});
-    iteration(i + 1, Flag<true>{});
+  for (;;) {
+    bool done = false;
+    static_for<2 * NR>([&](auto pc) __attribute__((always_inline)) {
+      constexpr int p = decltype(pc)::value;
+      if (!done) {
+        if constexpr (p % 2 == 0) body(SA, dPA, SB, dPB, PB, DSB, PA, DSA, i, pc);
+        else body(SB, dPB, SA, dPA, PA, DSA, PB, DSB, i, pc);
+        done = ++i == nsteps;
+      }
+    });
+    if (done) break;
   }
-  if (i < nsteps) iteration(i, Flag<false>{});
   // the S and dP of step nsteps (never used) are still being written: keep their registers
   // until the MFMAs are done
   mfma_fence();
@@ -808,7 +815,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // dV/dK of the last step (its rows are in slot (nsteps-1) % NR)
   {
     const bool odd_last = (nsteps - 1) & 1;
-    const uint32_t Ql = ring[0], dOl = Ql + QB;   // slot of step nsteps-1
+    const uint32_t Ql = (uint32_t)((nsteps - 1) % NR) * 2 * QB, dOl = Ql + QB;   // slot of step nsteps-1
     auto last = [&](const bf16x8 (&Pl)[2], const bf16x8 (&Sl)[2]) __attribute__((always_inline)) {
 #pragma unroll
       for (int u = 0; u < NT; ++u) {   // the first PF fragments were read by the last iteration
