@@ -521,7 +521,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     gdst[j] = (uint32_t)(tens * QB + ins * 1024);
   }
   const uint32_t hoff0 = (uint32_t)(hk * G) * RB, hst0 = (uint32_t)(hk * G) * (uint32_t)ns * 4;
-  // copy j of a step (head h, ring slot byte offset slot_off) into its ring slot
+  // copy j of a step (head offsets hoff/hst, ring slot byte offset slot_off) into its ring slot
   auto issue_one = [&](uint32_t slot_off, uint32_t hoff, const Rows& rw, int j) __attribute__((always_inline)) {
     copy16_to_lds_off(gsrc[j], rw.off[j] + hoff, smem_base + slot_off + gdst[j]);
   };
@@ -555,12 +555,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   };
 
   // steps whose rows may see only part of the tile ([mask_lo, mask_hi) of the list) or lie past
-  // the list: [s_lo, s_hi) and [s_pad, nsteps)
+  // the list lie in [s_lo, s_hi) or [s_pad, nsteps); the mask is applied from the first of them on
+  // (on a step whose rows see every key it changes nothing)
   const int s_lo = it.mask_lo / Q_SUB * G, s_hi = (it.mask_hi + Q_SUB - 1) / Q_SUB * G;
   const int s_pad = nq / Q_SUB * G;
-  auto is_masked = [&](int step) __attribute__((always_inline)) {
-    return (uint32_t)(step - s_lo) < (uint32_t)(s_hi - s_lo) || (step >= s_pad && step < nsteps);
-  };
+  const int s_mask = s_lo < s_hi ? min(s_lo, s_pad) : s_pad;
 
   // ---- iteration i, NSLOT MFMA slots (a pair of slots per fragment):
   //   pairs 0 .. NT-1: dV[nb] += P^T dO and dK[nb] += dS^T Q of step i-1 (pair u = DB*t2 + nb)
@@ -607,7 +606,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // the causal mask, on a step whose rows may see only part of the tile (or lie past the list,
   // position -1): a hidden (row, key) pair's S starts at -inf.  Every other step skips it.
   auto mask_acc = [&](f32x16& S, int step, int sub) __attribute__((always_inline)) {   // sub: step's subtile
-    if (is_masked(step)) {
+    if (step >= s_mask) {
       const int* qpp = &s_qpos[0][0] + (sub & 15) * Q_SUB;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -617,7 +616,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     }
   };
-  int h3, subc;                               // head and subtile of the copy step min(i+3, nsteps-1)
+  int h3, subc;                               // head of the copy step i+3 and subtile of min(i+3, nsteps-1)
   int h1 = 1 % G, sub1 = 1 / G;               // head and subtile of step i+1
   uint32_t hoff3, hst3;                       // its head offsets in Q/dO rows and in the statistics
   auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
@@ -639,15 +638,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
     bf16x8 fq[KS], fo[KS];
     auto load_frag = [&](int f) __attribute__((always_inline)) {
+      // (the operand of the pair's second MFMA is read first: the wait for the first covers both)
       if (f < NT) {
-        ftv[f] = ld_t(dOp, f);
         ftk[f] = ld_t(Qp, f);
+        ftv[f] = ld_t(dOp, f);
       } else if (f < NT + KS) {
-        fq[f - NT] = ld_a(Qn, f - NT);
         fo[f - NT] = ld_a(dOn, f - NT);
+        fq[f - NT] = ld_a(Qn, f - NT);
       } else if (f < NT + KS + PF) {
-        ftv[f - NT - KS] = ld_t(dOc, f - NT - KS);
         ftk[f - NT - KS] = ld_t(Qc, f - NT - KS);
+        ftv[f - NT - KS] = ld_t(dOc, f - NT - KS);
       }
     };
     // element v of this step's 16 per lane: scaled at F(v), exponentiated at F(v)+1, dS at
@@ -728,8 +728,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       h1 = wrap ? 0 : h1 + 1;
       sub1 += wrap ? 1 : 0;
     }
-    // the copy step advances to i+4 unless that is past the last step
-    if (i + NR - 1 < nsteps) {
+    // the copy step's head advances (past the last step the rows stay those of the last subtile,
+    // so any head still addresses rows of the list)
+    {
       const bool wrap = h3 == G - 1;
       h3 = wrap ? 0 : h3 + 1;
       hoff3 = wrap ? hoff0 : hoff3 + RB;
