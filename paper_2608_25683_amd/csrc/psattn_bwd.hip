@@ -432,7 +432,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   static_assert(SPB > NR + 2, "the first NR steps read row block 0; a buffer is refilled after its readers");
   static_assert(2 * SPB == 16 && IDX_BLK == SPB * Q_SUB, "subtile sub is staged at entry (sub & 15) * Q_SUB");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NR][2][QB];   // [step slot][Q | dO]
-  __shared__ __attribute__((aligned(16))) float s_stat[NR][2][Q_SUB];  // [step slot][-LSE/scale | -Delta]
+  __shared__ __attribute__((aligned(16))) uint32_t s_stat[NR][Q_SUB][2];  // [step slot][row][-LSE/scale | -Delta] as (hi, lo) bf16
   __shared__ int s_row[2][IDX_BLK];
   __shared__ int s_qpos[2][IDX_BLK];
   const uint32_t smem_base = lds_addr(&smem[0][0][0]), stat_base = lds_addr(&s_stat[0][0][0]);
@@ -493,11 +493,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // ---- copies.  Copy instruction j of this wave moves 16 bytes per lane of row r_j = ins*RPI + crow
   // of a subtile of tensor tens (Q or dO); its source byte offset is the lane's rowoff_j (row of the
   // list times hq*RB, plus the swizzled column: changes with the subtile) plus hoff = (hk*G + h)*RB
-  // (uniform: changes with the head).  Every wave also copies the step's -LSE/scale (lanes 0-31)
-  // and -Delta (lanes 32-63), the same 256 bytes, so that all waves issue and wait alike.
+  // (uniform: changes with the head).  Every wave also copies the step's -LSE/scale (even lanes)
+  // and -Delta (odd lanes) of its 32 rows, the same 256 bytes, so that all waves issue and wait
+  // alike.
   struct Rows {
     uint32_t off[CPS];   // rowoff_j
-    uint32_t st;         // 4 * row (+ the distance from the -LSE/scale to the -Delta array on lanes 32-63)
+    uint32_t st;         // 4 * row lane/2 (+ the distance from the -LSE/scale to the -Delta array on odd lanes)
   };
   const uint32_t nd_dist = (uint32_t)((const char*)a.kv_nd - (const char*)a.kv_nls);
   const uint32_t row_bytes = (uint32_t)hq * RB;
@@ -509,7 +510,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int r = ((wave + 4 * j) % NI) * RPI + crow;
       o.off[j] = (uint32_t)rows[r] * row_bytes + ((cpc ^ swz<D>(r)) << 4);
     }
-    o.st = (uint32_t)rows[l32] * 4 + (hh ? nd_dist : 0u);
+    o.st = (uint32_t)rows[lane >> 1] * 4 + ((lane & 1) ? nd_dist : 0u);
     return o;
   };
   const void* gsrc[CPS];                      // tensor of copy j
@@ -561,11 +562,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int s_pad = nq / Q_SUB * G;
   const int s_mask = s_lo < s_hi ? min(s_lo, s_pad) : s_pad;
 
-  // ---- iteration i, NSLOT MFMA slots (a pair of slots per fragment):
+  // ---- iteration i, NSLOT MFMA slots in NP pairs:
   //   pairs 0 .. NT-1: dV[nb] += P^T dO and dK[nb] += dS^T Q of step i-1 (pair u = DB*t2 + nb)
-  //   then:            S = Q K^T and dP = dO V^T of step i+1 (pair = k-step s)
+  //   pair NT:         S and dP of step i+1 start as -LSE/scale and -Delta (the statistics pair)
+  //   then:            S += Q K^T and dP += dO V^T of step i+1 (pair = k-step s)
   // with P and dS of step i computed between them.  Sc/dPc: step i; Sn/dPn: step i+1 (written);
-  // Pp/Sp: packed P and dS of step i-1; Pc/Sc2: of step i (written).
+  // Pp/Sp: packed P and dS of step i-1; Pc/Sc2: of step i (written).  S and dP thus leave the
+  // MFMAs as S - LSE/scale and dP - Delta: P = exp2(c S') and dS = P dP' take two VALU products.
+  // On a step whose rows may see only part of the tile, the causal mask sets S to -inf at the
+  // start of the iteration that consumes it.
   // Fragments are read PF pairs ahead of their MFMAs; the last pairs read the first PF dV/dK
   // fragments of iteration i+1 (step i's rows, long landed), so an iteration never starts with
   // an empty queue.  After slot BAR (MFMAs in flight) the wave waits for its copies of step i+1,
@@ -574,39 +579,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // boundary) the row offsets of the next subtile.  A row block is staged in the iteration that
   // fetches the rows of its first subtile; the buffer it overwrites last held the block before the
   // previous one, whose readers (at least SPB*G >= 8 steps earlier) are all past the last barrier.
-  // The S and dP accumulators of step i+1 are loaded with -LSE/scale and -Delta of its rows right
-  // after the barrier (and -inf where the causal mask hides a pair), so that the MFMAs leave
-  // S - LSE/scale and dP - Delta: P = exp2(c S') and dS = P dP' take two VALU products.
-  // The loop's bookkeeping is incremental and uniform: the ring of slot offsets rotates, and the
-  // copy step's head, head offsets and subtile advance by one step per iteration (frozen once the
-  // copies pass the last step: they then refill a slot no one reads).
+  // The loop's bookkeeping is incremental and uniform: the copy step's head, head offsets and
+  // subtile advance by one step per iteration (the rows freeze once the copies pass the last step:
+  // they then refill a slot no one reads).
   constexpr int NT = 2 * DB;                  // dV/dK slot pairs
   constexpr int PF = 3;
-  constexpr int NSLOT = 2 * NT + 2 * KS;
+  constexpr int NP = NT + 1 + KS;             // pairs: dV/dK, statistics, S/dP k-steps
+  constexpr int NSLOT = 2 * NP;
   constexpr int BAR = 2 * (NT - PF) - 1 < 3 ? 2 * (NT - PF) - 1 : 3;
   constexpr int CP0 = BAR + 1, CPD = 3;       // copy j of step i+3 at slot CP0 + CPD*j
   constexpr int ST_SLOT = CP0 + CPD * CPS, ROW_SLOT = ST_SLOT + 2;
-  constexpr int INIT_SLOT = BAR + 1, MASK_SLOT = 2 * NT - 3;
-  static_assert(BAR >= 1 && ROW_SLOT < NSLOT && INIT_SLOT + 1 < MASK_SLOT, "iteration schedule");
+  static_assert(BAR >= 1 && ROW_SLOT < NSLOT && 2 * (NT - PF) > BAR, "iteration schedule");
   bf16x8 ftv[NT], ftk[NT];                    // transposed dO and Q fragments of the dV/dK pairs
   Rows rows_nx;                               // row offsets of the copy step's subtile
-  // element v of a step's S and dP (row 8*(v/4) + 4*hh + v%4) starts at -LSE/scale and -Delta
-  auto init_acc = [&](f32x16& S, f32x16& dP, uint32_t slot_off, auto part) __attribute__((always_inline)) {
-    const float* st = &s_stat[0][0][0] + slot_off / (2 * QB) * (2 * Q_SUB);
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 x = *(const f32x4*)&st[decltype(part)::value * Q_SUB + 8 * g + 4 * hh];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if constexpr (decltype(part)::value == 0) S[4 * g + k] = x[k];
-        else dP[4 * g + k] = x[k];
-      }
-    }
+  // The statistics pair: S and dP of a step start as MFMAs of A = (hi, lo) of the row's -LSE/scale
+  // and (hi, lo) of its -Delta, each split into two bf16 (relative error 2^-16), in k = 0..3, with
+  // B = (1, 1, 0, 0, ...) or (0, 0, 1, 1, 0, ...) on every key: one 64-bit LDS read per lane
+  // instead of 32 values.  B is zero on lanes 32-63 (k = 8..15), where A repeats the row's pairs.
+  bf16x8 bs1 = as_bf(hh ? u32x4{0u, 0u, 0u, 0u} : u32x4{0x3F803F80u, 0u, 0u, 0u});
+  bf16x8 bd1 = as_bf(hh ? u32x4{0u, 0u, 0u, 0u} : u32x4{0u, 0x3F803F80u, 0u, 0u});
+  pin_a(bs1);
+  pin_a(bd1);
+  auto ld_stat = [&](uint32_t slot_off) __attribute__((always_inline)) {
+    const uint32_t* st = &s_stat[0][0][0] + slot_off / (2 * QB) * (2 * Q_SUB);
+    const u32x2 x = ld8(st + 2 * l32);
+    return as_bf(u32x4{x[0], x[1], 0u, 0u});
   };
   // the causal mask, on a step whose rows may see only part of the tile (or lie past the list,
-  // position -1): a hidden (row, key) pair's S starts at -inf.  Every other step skips it.
-  auto mask_acc = [&](f32x16& S, int step, int sub) __attribute__((always_inline)) {   // sub: step's subtile
+  // position -1): S of a hidden (row, key) pair becomes -inf before its exponential.  Every
+  // other step skips it.
+  auto mask_s = [&](f32x16& S, int step, int sub) __attribute__((always_inline)) {   // sub: step's subtile
     if (step >= s_mask) {
+      mfma_fence();   // S was written by MFMAs of the previous iteration
       const int* qpp = &s_qpos[0][0] + (sub & 15) * Q_SUB;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -617,7 +621,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
   };
   int h3, subc;                               // head of the copy step i+3 and subtile of min(i+3, nsteps-1)
-  int h1 = 1 % G, sub1 = 1 / G;               // head and subtile of step i+1
+  int h0 = 0, sub0 = 0;                       // head and subtile of step i
   uint32_t hoff3, hst3;                       // its head offsets in Q/dO rows and in the statistics
   auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
                   bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i, auto pos) __attribute__((always_inline)) {
@@ -636,18 +640,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       s_row[blk & 1][tid] = pre_row;
       s_qpos[blk & 1][tid] = pre_qpos;
     }
-    bf16x8 fq[KS], fo[KS];
-    auto load_frag = [&](int f) __attribute__((always_inline)) {
+    bf16x8 fq[KS], fo[KS], ast;
+    auto load_frag = [&](int f) __attribute__((always_inline)) {   // operands of pair f
       // (the operand of the pair's second MFMA is read first: the wait for the first covers both)
       if (f < NT) {
         ftk[f] = ld_t(Qp, f);
         ftv[f] = ld_t(dOp, f);
-      } else if (f < NT + KS) {
-        fo[f - NT] = ld_a(dOn, f - NT);
-        fq[f - NT] = ld_a(Qn, f - NT);
-      } else if (f < NT + KS + PF) {
-        ftk[f - NT - KS] = ld_t(Qc, f - NT - KS);
-        ftv[f - NT - KS] = ld_t(dOc, f - NT - KS);
+      } else if (f == NT) {
+        ast = ld_stat(Qn);
+      } else if (f <= NT + KS) {
+        fo[f - NT - 1] = ld_a(dOn, f - NT - 1);
+        fq[f - NT - 1] = ld_a(Qn, f - NT - 1);
+      } else if (f < NP + PF) {
+        ftk[f - NP] = ld_t(Qc, f - NP);
+        ftv[f - NP] = ld_t(dOc, f - NP);
       }
     };
     // element v of this step's 16 per lane: scaled at F(v), exponentiated at F(v)+1, dS at
@@ -686,13 +692,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     auto slot = [&](auto ic) __attribute__((always_inline)) {
       constexpr int si = decltype(ic)::value;
       constexpr int m = si / 2, w = si % 2;
+      if constexpr (si == 0) mask_s(Sc, i, sub0);
       if constexpr (w == 0) load_frag(m + PF);
-      if constexpr (si < 2 * NT) {
+      if constexpr (m < NT) {
         constexpr int t2 = m / DB, nb = m % DB;
         if constexpr (w == 0) mma_a(dv[nb], Pp[t2], ftv[m]);
         else mma_a(dk[nb], Sp[t2], ftk[m]);
+      } else if constexpr (m == NT) {
+        if constexpr (w == 0) mma_v_first(Sn, ast, bs1);
+        else mma_v_first(dPn, ast, bd1);
       } else {
-        constexpr int s = m - NT;
+        constexpr int s = m - NT - 1;
         if constexpr (w == 0) mma_v(Sn, fq[s], kreg[s]);
         else mma_v(dPn, fo[s], vreg[s]);
       }
@@ -702,9 +712,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         if (new_blk) wait_lds<0>();   // the staged row block is written before the barrier
         barrier_only();
       }
-      if constexpr (si == INIT_SLOT) init_acc(Sn, dPn, Qn, IntC<0>{});
-      if constexpr (si == INIT_SLOT + 1) init_acc(Sn, dPn, Qn, IntC<1>{});
-      if constexpr (si == MASK_SLOT) mask_acc(Sn, i + 1, sub1);
       if constexpr (si >= CP0 && si < CP0 + CPD * CPS && (si - CP0) % CPD == 0) issue_one(slot3, hoff3, rows_nx, (si - CP0) / CPD);
       if constexpr (si == ST_SLOT) issue_stat(slot3, hst3, rows_nx);
       if constexpr (si == ROW_SLOT) {
@@ -724,9 +731,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     };
     static_for<NSLOT>(slot);
     {
-      const bool wrap = h1 == G - 1;
-      h1 = wrap ? 0 : h1 + 1;
-      sub1 += wrap ? 1 : 0;
+      const bool wrap = h0 == G - 1;
+      h0 = wrap ? 0 : h0 + 1;
+      sub0 += wrap ? 1 : 0;
     }
     // the copy step's head advances (past the last step the rows stay those of the last subtile,
     // so any head still addresses rows of the list)
@@ -767,10 +774,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // add nothing); the first dV/dK fragments of iteration 0 (step 0's rows)
   {
     const uint32_t Q0 = 0, dO0 = QB;
-    init_acc(SA, dPA, 0, IntC<0>{});
-    init_acc(SA, dPA, 0, IntC<1>{});
-    mask_acc(SA, 0, 0);
+    bf16x8 a0 = ld_stat(0);
+    anchor(a0);
     valu_fence();
+    mma_v_first(SA, a0, bs1);
+    mma_v_first(dPA, a0, bd1);
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       mma_v(SA, ld_a(Q0, s), kreg[s]);
@@ -1369,8 +1377,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
     const size_t o = (size_t)h * a.s.ns + row;
     a.delta[o] = acc;
     a.lse2[o] = a.LSE[o] * kLog2e;
-    a.kv_nls[o] = -a.LSE[o] / a.s.scale;
-    a.kv_nd[o] = -acc;
+    ((uint32_t*)a.kv_nls)[o] = split_bf16(-a.LSE[o] / a.s.scale);
+    ((uint32_t*)a.kv_nd)[o] = split_bf16(-acc);
   }
 }
 

@@ -58,6 +58,11 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 __device__ __forceinline__ float bf2f(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+// x as hi + lo, two bf16 (hi the nearest bf16 to x, lo the nearest to x - hi), hi in the low half
+__device__ __forceinline__ uint32_t split_bf16(float x) {
+  const float hi = bf2f(pack2(x, 0.f) & 0xffffu);
+  return pack2(x, x - hi);
+}
 // 8 consecutive accumulator values -> one bf16x8 MFMA operand
 __device__ __forceinline__ bf16x8 pack8(const f32x16& x, int base) {
   u32x4 w;
