@@ -426,10 +426,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr int NI = Q_SUB / RPI;             // copy instructions per subtile and tensor
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int SPB = IDX_BLK / Q_SUB;        // subtiles per staged row block
-  constexpr int NR = 5;                       // step ring: steps i-1 .. i+3
+  constexpr int NR = 5;                       // step ring: steps i-1 .. i+NR-2 (copied NR-2 ahead)
   constexpr int CPS = 2 * NI / 4;             // copies every wave issues per step (Q and dO)
   static_assert((2 * NI) % 4 == 0 && (1 << LRB) == RB, "copy split");
-  static_assert(SPB > NR + 2, "the first NR steps read row block 0; a buffer is refilled after its readers");
+  static_assert(SPB > NR + 1, "the first NR steps read row block 0; a buffer is refilled after its readers");
+  constexpr int PER = NR % 2 == 0 ? NR : 2 * NR;   // loop trip: the S/dP buffers alternate with period 2
   static_assert(2 * SPB == 16 && IDX_BLK == SPB * Q_SUB, "subtile sub is staged at entry (sub & 15) * Q_SUB");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NR][2][QB];   // [step slot][Q | dO]
   __shared__ __attribute__((aligned(16))) uint32_t s_stat[NR][Q_SUB][2];  // [step slot][row][-LSE/scale | -Delta] as (hi, lo) bf16
@@ -625,7 +626,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   uint32_t hoff3, hst3;                       // its head offsets in Q/dO rows and in the statistics
   auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
                   bf16x8 (&Pc)[2], bf16x8 (&Sc2)[2], int i, auto pos) __attribute__((always_inline)) {
-    // pos = i mod 2*NR: the ring slots of steps i-1, i, i+1 and i+3 are compile-time constants, so
+    // pos = i mod PER: the ring slots of steps i-1, i, i+1 and i+NR-2 are compile-time constants, so
     // that a read address is an immediate offset from the lane's base (step -1 reads ring slot
     // NR-1, zero-filled before the loop, with zero P and dS)
     constexpr int p = decltype(pos)::value;
@@ -708,7 +709,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
       chunk(ic);
       if constexpr (si == BAR) {
-        wait_vmem<CPS + 1>();
+        wait_vmem<(NR - 4) * (CPS + 1)>();
         if (new_blk) wait_lds<0>();   // the staged row block is written before the barrier
         barrier_only();
       }
@@ -798,12 +799,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     mfma_fence();
   }
 
-  // 2*NR iterations per trip (the S/dP buffers alternate with period 2, the ring with period NR),
+  // PER iterations per trip (the S/dP buffers alternate with period 2, the ring with period NR),
   // leaving after whichever iteration is the last
   int i = 0;
   for (;;) {
     bool done = false;
-    static_for<2 * NR>([&](auto pc) __attribute__((always_inline)) {
+    static_for<PER>([&](auto pc) __attribute__((always_inline)) {
       constexpr int p = decltype(pc)::value;
       if (!done) {
         if constexpr (p % 2 == 0) body(SA, dPA, SB, dPB, PB, DSB, PA, DSA, i, pc);
