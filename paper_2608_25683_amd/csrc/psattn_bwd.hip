@@ -657,10 +657,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         ftv[f - NP] = ld_t(dOc, f - NP);
       }
     };
-    // element v of this step's 16 per lane: scaled at F(v), exponentiated at F(v)+1, dS at
-    // F(v)+2; each 8-element half packed after its last one
+    // element v of this step's 16 per lane: scaled at F(v), exponentiated at F(v)+2 (a slot of
+    // other work between the product and the exponential that reads it, so that no wait states are
+    // padded), dS at F(v)+3; each 8-element half packed after its last one
     constexpr auto F = [](int v) { return 2 + (v * (NSLOT - 8)) / 16; };
-    static_assert(F(15) + 3 < NSLOT, "P and dS packed within the iteration");
+    static_assert(F(15) + 4 < NSLOT, "P and dS packed within the iteration");
     auto chunk = [&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
       static_for<16>([&](auto vc) __attribute__((always_inline)) {
@@ -672,17 +673,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           anchor(t);
           Sc[v] = t;
         }
-        if constexpr (F(v) + 1 == q) {
+        if constexpr (F(v) + 2 == q) {
           float t = fast_exp2(Sc[v]);
           anchor(t);
           Sc[v] = t;
         }
-        if constexpr (F(v) + 2 == q) {
+        if constexpr (F(v) + 3 == q) {
           float t = Sc[v] * dPc[v];
           anchor(t);
           dPc[v] = t;
         }
-        if constexpr (v % 8 == 7 && F(v) + 3 == q) {
+        if constexpr (v % 8 == 7 && F(v) + 4 == q) {
           Pc[v / 8] = pack8(Sc, 8 * (v / 8));
           Sc2[v / 8] = pack8(dPc, 8 * (v / 8));
           anchor(Pc[v / 8]);
