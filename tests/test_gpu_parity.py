@@ -38,7 +38,7 @@ def test_random_forest_forced_splits(seed):
     H.check_full(wl, H.run_gpu(wl, opts={"fwd_kv_split": 64, "bwd_q_chunk": 32}), H.run_oracle(wl))
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(5, 1, 128), (8, 8, 64), (2, 1, 64), (12, 2, 128), (16, 2, 64), (3, 1, 128)])
+@pytest.mark.parametrize("hq,hkv,d", [(5, 1, 128), (8, 8, 64), (2, 1, 64), (12, 2, 128), (16, 2, 64), (3, 1, 128), (16, 1, 128)])
 def test_head_layouts(hq, hkv, d):
     wl = W.random_forest(400 + hq, max_nodes=5, max_seg=70, hq=hq, hkv=hkv, d=d, dtype="bf16")
     _say(f"head layout hq={hq} hkv={hkv} d={d}")
