@@ -960,8 +960,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   auto issue_slots = [&](int t, int (&slot)[IPW]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
-      const int key = min(t * KV_TILE + (wave + NW * i) * RPI + crow, nkv - 1);
-      slot[i] = s_slot[(key / IDX_BLK) & 1][key % IDX_BLK];
+      // the two staged blocks are contiguous: entry key sits at key mod 2*IDX_BLK
+      const uint32_t key = (uint32_t)min(t * KV_TILE + (wave + NW * i) * RPI + crow, nkv - 1);
+      slot[i] = (&s_slot[0][0])[key & (2 * IDX_BLK - 1)];
     }
   };
   auto issue_copy1 = [&](int rs, int i, int slot, int tensor) __attribute__((always_inline)) {
