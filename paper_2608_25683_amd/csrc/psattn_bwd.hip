@@ -944,43 +944,48 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     }
   }
 
-  const int koff0 = tile_off<D>(l32, hh);                  // K/V rows l32, chunk 2s + hh: koff0 ^ (s << 5)
-  int toff[2];                                             // K^T reads, d block mb: toff ^ (mb << 6)
+  // LDS byte offsets of this lane's fragments inside a 32-key block (gtile_off layout): K or V
+  // fragment s (rows l32, chunk 2s + hh) at koff[s & 1] + 1024 (s >> 1); K^T fragment of k-step
+  // t2 and d block mb (rows 16 t2 + 8 rd + 4 hh + r4, chunks 4 mb + (dsub + 4 j) / 8) at
+  // toff[rd] + 16 t2 RB + 1024 mb
+  const int koff[2] = {gtile_off<D>(l32, hh), gtile_off<D>(l32, 2 + hh)};
+  int toff[2];
   {
     const int r4 = (lane & 15) >> 2, j = lane & 3, dsub = 16 * ((lane >> 4) & 1);
 #pragma unroll
-    for (int rd = 0; rd < 2; ++rd) toff[rd] = tile_off<D>(8 * rd + 4 * hh + r4, (dsub + 4 * j) >> 3) + 8 * (j & 1);
+    for (int rd = 0; rd < 2; ++rd) toff[rd] = gtile_off<D>(8 * rd + 4 * hh + r4, (dsub + 4 * j) >> 3) + 8 * (j & 1);
   }
+  static_assert(NW == 4 && IPW == D / 32, "copies: wave w fills row group w of a tile, IPW units per tensor");
 
   const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
   const uint8_t* Kb = (const uint8_t*)a.K + (size_t)hk * D * sizeof(bf16_t);
   const uint8_t* Vb = (const uint8_t*)a.V + (size_t)hk * D * sizeof(bf16_t);
-  const int crow = lane / CPR, cpc = lane % CPR;
-  const uint32_t smem_base = lds_addr(&smem[0][0][0]);
-  auto issue_slots = [&](int t, int (&slot)[IPW]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      // the two staged blocks are contiguous: entry key sits at key mod 2*IDX_BLK
-      const uint32_t key = (uint32_t)min(t * KV_TILE + (wave + NW * i) * RPI + crow, nkv - 1);
-      slot[i] = (&s_slot[0][0])[key & (2 * IDX_BLK - 1)];
-    }
+  // Copies: wave w fills row group w (keys 16 w .. 16 w + 15) of every tile, one 1 KB unit
+  // (chunks 4 i .. 4 i + 3) per instruction i.  Lane l writes chunk 4 i + l / 16 of the row at
+  // position l % 16, i.e. of key row (l % 16) ^ 4 (l / 16) of the group.
+  const int crow = 16 * wave + ((lane & 15) ^ (4 * (lane >> 4)));
+  const uint32_t cbyte = (uint32_t)(lane >> 4) << 4;
+  const uint32_t smem_base = lds_addr(&smem[0][0][0]) + wave * 16 * RB;
+  // the slot of this lane's copy row in key tile t (the two staged index blocks are contiguous:
+  // entry key sits at key mod 2*IDX_BLK)
+  auto issue_slot = [&](int t) __attribute__((always_inline)) {
+    const uint32_t key = (uint32_t)min(t * KV_TILE + crow, nkv - 1);
+    return (&s_slot[0][0])[key & (2 * IDX_BLK - 1)];
   };
-  auto issue_copy1 = [&](int rs, int i, int slot, int tensor) __attribute__((always_inline)) {
-    const int k = wave + NW * i;
-    const int r = k * RPI + crow;
-    const uint32_t dst = smem_base + (uint32_t)((rs * 2 + tensor) * TB) + k * 1024;
-    const uint32_t off = __umul24((uint32_t)slot, kv_stride) + ((cpc ^ swz<D>(r)) << 4);
-    copy16_to_lds_off(tensor ? Vb : Kb, off, dst);
+  // copy instruction i of a tile into ring slot rs, K (tensor 0) or V (tensor 1)
+  auto issue_copy1 = [&](int rs, auto ic, int slot, int tensor) __attribute__((always_inline)) {
+    constexpr int i = decltype(ic)::value;
+    const uint32_t dst = smem_base + (uint32_t)((rs * 2 + tensor) * TB) + i * 1024;
+    const uint32_t off = __umul24((uint32_t)slot, kv_stride) + cbyte;
+    copy16_to_lds_off_imm<64 * i>(tensor ? Vb : Kb, off, dst);
   };
   // all copies into ring slot t % NS, of tile min(t, ntiles - 1) (see the forward kernel)
   auto issue = [&](int t) __attribute__((always_inline)) {
-    int slot[IPW];
-    issue_slots(min(t, ntiles - 1), slot);
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      issue_copy1(t % NS, i, slot[i], 0);
-      issue_copy1(t % NS, i, slot[i], 1);
-    }
+    const int slot = issue_slot(min(t, ntiles - 1));
+    static_for<IPW>([&](auto ic) __attribute__((always_inline)) {
+      issue_copy1(t % NS, ic, slot, 0);
+      issue_copy1(t % NS, ic, slot, 1);
+    });
   };
   auto fetch_index_block = [&](int b) __attribute__((always_inline)) {
     if (b * IDX_BLK >= nkv) return;
@@ -1038,13 +1043,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     static_assert(F(31) + 2 <= 31, "dS schedule");
     bf16x8 kf[KS], vf[KS], tf[NDQ];
     auto load_k = [&](int s) __attribute__((always_inline)) {
-      kf[s] = as_bf(ld16(Kn + (koff0 ^ (s << 5))));
-      vf[s] = as_bf(ld16(Vn + (koff0 ^ (s << 5))));
+      kf[s] = as_bf(ld16(Kn + koff[s & 1] + (s >> 1) * 1024));
+      vf[s] = as_bf(ld16(Vn + koff[s & 1] + (s >> 1) * 1024));
     };
     auto load_t = [&](int u) __attribute__((always_inline)) {   // u = DB * t2 + mb
       const int t2 = u / DB, mb = u % DB;
-      const uint8_t* kp = Kp + 16 * t2 * RB;
-      tf[u] = as_bf(lds_tr(kp + (toff[0] ^ (mb << 6))), lds_tr(kp + (toff[1] ^ (mb << 6))));
+      const int o = 16 * t2 * RB + 1024 * mb;
+      tf[u] = as_bf(lds_tr(Kp + toff[0] + o), lds_tr(Kp + toff[1] + o));
     };
     // fragments in use order: (K, V) pairs of the S and dP MFMAs and K^T fragments of the dQ
     // MFMAs, in the order the stage issues them; each is read PF pairs ahead
@@ -1106,8 +1111,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     const uint8_t* V0 = &smem[0][1][0];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      const bf16x8 k = as_bf(ld16(K0 + (koff0 ^ (s << 5))));
-      const bf16x8 v = as_bf(ld16(V0 + (koff0 ^ (s << 5))));
+      const bf16x8 k = as_bf(ld16(K0 + koff[s & 1] + (s >> 1) * 1024));
+      const bf16x8 v = as_bf(ld16(V0 + koff[s & 1] + (s >> 1) * 1024));
 #pragma unroll
       for (int rh = 0; rh < 2; ++rh) {
         if (s == 0) {
@@ -1134,11 +1139,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     const uint8_t* Vt = &smem[t % NS][1][0];
     const uint8_t* Kprev = t > 0 ? &smem[(t + NS - 1) % NS][0][0] + 32 * RB : Kt;
     const int tn = t + NS - 1;
-    int slot[IPW];
-    issue_slots(min(tn, ntiles - 1), slot);
+    const int slot = issue_slot(min(tn, ntiles - 1));
     auto vcopies = [&](auto ic) __attribute__((always_inline)) {
       constexpr int i = decltype(ic)::value;
-      if constexpr (i % 6 == 3 && i / 6 < IPW) issue_copy1(tn % NS, i / 6, slot[i / 6], 1);
+      if constexpr (i % 6 == 3 && i / 6 < IPW) issue_copy1(tn % NS, IntC<i / 6>{}, slot, 1);
     };
     // stage 2t: S, dP of block 2t+1, dQ of block 2t-1, dS of block 2t; V copies
     stage(SA, dPA, SB, dPB, dSB, dSA, Kt + 32 * RB, Vt + 32 * RB, Kprev, t * KV_TILE, masked, vcopies, Flag<false>{});
@@ -1146,7 +1150,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     __syncthreads();
     auto kcopies = [&](auto ic) __attribute__((always_inline)) {
       constexpr int i = decltype(ic)::value;
-      if constexpr (i % 6 == 3 && i / 6 < IPW) issue_copy1(tn % NS, i / 6, slot[i / 6], 0);
+      if constexpr (i % 6 == 3 && i / 6 < IPW) issue_copy1(tn % NS, IntC<i / 6>{}, slot, 0);
       if constexpr (i == 6 * IPW + 3) {
         if (tn < ntiles && tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
       }
@@ -1166,8 +1170,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 #pragma unroll
     for (int u = 0; u < NDQ; ++u) {
       const int t2 = u / DB, mb = u % DB;
-      const uint8_t* kp = Kl + 16 * t2 * RB;
-      const bf16x8 k = as_bf(lds_tr(kp + (toff[0] ^ (mb << 6))), lds_tr(kp + (toff[1] ^ (mb << 6))));
+      const int o = 16 * t2 * RB + 1024 * mb;
+      const bf16x8 k = as_bf(lds_tr(Kl + toff[0] + o), lds_tr(Kl + toff[1] + o));
       mma_a(dq[0][mb], k, dSB[0][t2]);
       mma_a(dq[1][mb], k, dSB[1][t2]);
     }

@@ -98,6 +98,18 @@ __device__ __forceinline__ int tile_off(int r, int c) {
   return r * (D * 2) + ((c ^ swz<D>(r)) << 4);
 }
 
+// ---- LDS tiles of the one-wavefront-per-SIMD kernels (rows of D bf16).  Rows come in groups
+// of 16.  A group is stored as 1 KB units, one per 4 consecutive 16-byte chunks: inside a unit
+// the chunks follow each other (256 bytes apiece) and row r of chunk c sits at position
+// (r mod 16) ^ 4 (c mod 4).  One copy instruction (64 lanes x 16 bytes) thus fills one unit with
+// 64 bytes of each of 16 rows.  Reads of one chunk by 16 consecutive rows, and the transposing
+// reads (4 rows x 4 chunks per 16 lanes, two such groups per 32 lanes), hit distinct banks, and
+// the chunk offset of a fragment splits into a per-lane part and a multiple of 1 KB.
+template <int D>
+__device__ __forceinline__ int gtile_off(int r, int c) {
+  return (r >> 4) * (16 * D * 2) + (c >> 2) * 1024 + (c & 3) * 256 + (((r & 15) ^ (4 * (c & 3))) << 4);
+}
+
 // 16 bytes per lane from global memory straight into LDS: lane i writes lds_base + 16 i.
 // Issued through inline assembly so that the compiler does not wait for the copy before every
 // later LDS read (it cannot tell which LDS bytes the copy writes); the kernels wait explicitly
@@ -114,6 +126,16 @@ __device__ __forceinline__ void copy16_to_lds_at(const void* g, uint32_t lds) {
 // 32-bit byte offset per lane).
 __device__ __forceinline__ void copy16_to_lds_off(const void* base, uint32_t off, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+// As copy16_to_lds_off, reading at base + off + OFF (OFF a compile-time byte offset), lane i
+// still writing lds + 16 i.  The instruction offset is added to the LDS address as well as to the
+// global one, so M0 is set to lds - OFF (lds >= OFF).
+template <int OFF>
+__device__ __forceinline__ void copy16_to_lds_off_imm(const void* base, uint32_t off, uint32_t lds) {
+  static_assert(OFF >= 0 && OFF < 4096, "global instruction offset range");
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3" ::"v"(off), "s"(base), "s"(lds - OFF),
+               "i"(OFF)
+               : "memory", "m0");
 }
 // LDS byte address of a pointer into a __shared__ array (the low half of its generic address).
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
