@@ -17,6 +17,10 @@
 #ifndef PSATTN_FWD_NS
 #define PSATTN_FWD_NS 4
 #endif
+// 32-row halves per wavefront of the main bf16 kernel: 2 (one wavefront per SIMD) or 1 (two)
+#ifndef PSATTN_FWD_NH
+#define PSATTN_FWD_NH 1
+#endif
 #ifndef PSATTN_FWD_PF
 #define PSATTN_FWD_PF 4
 #endif
@@ -228,16 +232,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 }
 
 // ============================================================================================
-// bf16 main kernel, 64 rows per wavefront.  One wavefront per SIMD (up to 512 registers), so a
-// wave holds the queries (AGPRs), the output accumulators (AGPRs) and the scores (VGPRs) of 64
-// rows -- two 32-row halves -- of one head: every K or V fragment read from LDS feeds two MFMAs,
-// half the LDS traffic per flop of a 32-row wave.  Work proceeds in 32-key blocks j; stage j
-// issues the score MFMAs of block j+1 and the PV MFMAs of block j-1, and between them the
-// softmax of block j (its scores were finished during stage j-1).  The instruction order inside
-// a stage is fixed (scheduling fences), so the VALU softmax runs in the shadow of the MFMAs.
-// Key tiles (two blocks) come through an NS-stage LDS ring, one barrier per tile.
-template <int D, int NW, int NS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_bf16_w64_kernel(FwdArgs a) {
+// bf16 main kernel.  A wavefront holds the queries (AGPRs), the output accumulators (AGPRs) and
+// the scores (VGPRs) of NH 32-row halves of one head.  NH = 2: one wavefront per SIMD (up to 512
+// registers), every K or V fragment read from LDS feeds two MFMAs.  NH = 1: eight wavefronts, two
+// per SIMD (up to 256 registers each), so one wavefront's softmax issues while the other's MFMAs
+// run, at twice the LDS reads per flop; measured the faster of the two on long prefixes.  Work
+// proceeds in 32-key blocks j; stage j issues the score MFMAs of block j+1 and the PV MFMAs of
+// block j-1, and between them the softmax of block j (its scores were finished during stage
+// j-1).  The instruction order inside a stage is fixed (scheduling fences).  Key tiles (two
+// blocks) come through an NS-stage LDS ring, one barrier per tile.
+template <int D, int NW, int NS, int NH>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH, 3 - NH))) void fwd_bf16_w64_kernel(FwdArgs a) {
   constexpr int RB = D * 2;
   constexpr int CPR = D / 8;
   constexpr int RPI = 64 / CPR;
@@ -257,8 +262,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int rw2 = a.s.rw >> 1;                   // 64-row blocks per head
-  const int head = it.head0 + wave / rw2;
+  const int rwn = a.s.rw / NH;                   // NH*32-row blocks per head
+  const int head = it.head0 + wave / rwn;
   const int hk = it.head0 / a.s.g;
   const int nkv = it.nkv;
   const int* kvl = a.plan.kv_list + it.kv_off;
@@ -269,12 +274,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     if (nkv > IDX_BLK) s_slot[1][i] = kvl[min(IDX_BLK + i, nkv - 1)];
   }
 
-  int ridx[2], row[2], lim[2];
-  bool row_ok[2];
-  bf16x8 qreg[2][KS];
+  int ridx[NH], row[NH], lim[NH];
+  bool row_ok[NH];
+  bf16x8 qreg[NH][KS];
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh) {
-    ridx[rh] = (wave % rw2) * 64 + 32 * rh + l32;
+  for (int rh = 0; rh < NH; ++rh) {
+    ridx[rh] = (wave % rwn) * (32 * NH) + 32 * rh + l32;
     row_ok[rh] = ridx[rh] < it.nq;
     row[rh] = a.plan.q_list[it.q_off + (row_ok[rh] ? ridx[rh] : it.nq - 1)];
     // key kidx of this item is visible to the row iff kidx <= lim
@@ -296,19 +301,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     for (int rd = 0; rd < 2; ++rd) voff[rd] = gtile_off<D>(8 * rd + 4 * hh + r4, (dsub + 4 * j) >> 3) + 8 * (j & 1);
   }
   static_assert(D == 128 || D == 64, "head_dim");
-  static_assert(NW == 4 && IPW == D / 32, "copies: wave w fills row group w of a tile, IPW units per tensor");
+  static_assert(NW * NH == 8 && IPW * NW == CPR, "copies: NW / 4 waves per row group of a tile, IPW units each");
 
   // pool rows are addressed by 32-bit byte offsets from the head's base (the launcher checks that
   // the pools are under 4 GiB and 2^24 rows, so slot * kv_stride is one 24-bit multiply-add)
   const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
   const uint8_t* Kb = (const uint8_t*)a.K + (size_t)hk * D * sizeof(bf16_t);
   const uint8_t* Vb = (const uint8_t*)a.V + (size_t)hk * D * sizeof(bf16_t);
-  // Copies: wave w fills row group w (keys 16 w .. 16 w + 15) of every tile, one 1 KB unit
-  // (chunks 4 i .. 4 i + 3) per instruction i.  Lane l writes chunk 4 i + l / 16 of the row at
-  // position l % 16, i.e. of key row (l % 16) ^ 4 (l / 16) of the group.
-  const int crow = 16 * wave + ((lane & 15) ^ (4 * (lane >> 4)));
-  const uint32_t cbyte = (uint32_t)(lane >> 4) << 4;
-  const uint32_t smem_base = lds_addr(&smem[0][0][0]) + wave * 16 * RB;
+  // Copies: row group cg = wave / (NW/4) (keys 16 cg .. 16 cg + 15) of every tile is filled by
+  // NW/4 waves, wave w taking the IPW 1 KB units u0 + i, u0 = IPW (w mod NW/4), one per
+  // instruction i (unit u holds chunks 4u .. 4u + 3).  Lane l writes chunk 4u + l / 16 of the
+  // row at position l % 16, i.e. of key row (l % 16) ^ 4 (l / 16) of the group.
+  const int cg = wave / (NW / 4), u0 = (wave % (NW / 4)) * IPW;
+  const int crow = 16 * cg + ((lane & 15) ^ (4 * (lane >> 4)));
+  const uint32_t cbyte = ((uint32_t)(lane >> 4) << 4) + 64 * u0;
+  const uint32_t smem_base = lds_addr(&smem[0][0][0]) + cg * 16 * RB + u0 * 1024;
   // the slot of this lane's copy row in key tile t (the two staged index blocks are contiguous:
   // entry key sits at key mod 2*IDX_BLK)
   auto issue_slot = [&](int t) __attribute__((always_inline)) {
@@ -337,20 +344,25 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
   };
 
-  f32x16 oacc[2][DB];
+  f32x16 oacc[NH][DB];
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh)
+  for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
     for (int mb = 0; mb < DB; ++mb) {
       oacc[rh][mb] = f32x16{};
       pin_a(oacc[rh][mb]);
     }
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh)
+  for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
     for (int s = 0; s < KS; ++s) pin_a(qreg[rh][s]);
   valu_fence();
-  float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
+  float m_run[NH], l_run[NH];
+#pragma unroll
+  for (int rh = 0; rh < NH; ++rh) {
+    m_run[rh] = kNegInf;
+    l_run[rh] = 0.f;
+  }
   const float c = a.s.scale * kLog2e;
   const float th = 8.f / c;
 
@@ -363,40 +375,40 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   // grows by more than 2^8 (always the case for the first block of a row) sends the whole wave
   // down a slow path after the stage: block j's scores are recomputed from Kc, exponentiated
   // against the new max, and O and the running sum are rescaled.
-  auto scores = [&](const uint8_t* Kb_, f32x16 (&S)[2]) __attribute__((always_inline)) {
+  auto scores = [&](const uint8_t* Kb_, f32x16 (&S)[NH]) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const bf16x8 k = as_bf(ld16(Kb_ + koff[s & 1] + (s >> 1) * 1024));
 #pragma unroll
-      for (int rh = 0; rh < 2; ++rh) {
+      for (int rh = 0; rh < NH; ++rh) {
         if (s == 0) mma_v_first(S[rh], k, qreg[rh][s]);
         else mma_v(S[rh], k, qreg[rh][s]);
       }
     }
   };
-  auto mask_elem = [&](f32x16 (&S)[2], int rh, int v, int kb) __attribute__((always_inline)) {
+  auto mask_elem = [&](f32x16 (&S)[NH], int rh, int v, int kb) __attribute__((always_inline)) {
     // element v holds key kb + 4*hh + 8*(v/4) + v%4, visible iff it is <= lim
     const int x = lim[rh] - kb - 4 * hh;
     S[rh][v] = (8 * (v >> 2) + (v & 3) > x) ? kNegInf : S[rh][v];
   };
-  auto stage = [&](f32x16 (&Sc)[2], f32x16 (&Sn)[2], const bf16x8 (&Pp)[2][2], bf16x8 (&Pc)[2][2],
+  auto stage = [&](f32x16 (&Sc)[NH], f32x16 (&Sn)[NH], const bf16x8 (&Pp)[NH][2], bf16x8 (&Pc)[NH][2],
                    const uint8_t* Kc, const uint8_t* Kn, const uint8_t* Vp, int kb, auto masked,
                    auto extra, auto pv_first) __attribute__((always_inline)) {
-    float mx[2], mt[2], ps[2][2], l_prev[2], mc[2];
-    bool g[2];
+    float mx[NH], mt[NH], ps[NH][2], l_prev[NH], mc[NH];
+    bool g[NH];
 #pragma unroll
-    for (int rh = 0; rh < 2; ++rh) mc[rh] = m_run[rh] == kNegInf ? 0.f : m_run[rh] * c;
+    for (int rh = 0; rh < NH; ++rh) mc[rh] = m_run[rh] == kNegInf ? 0.f : m_run[rh] * c;
     // element e = 16 rh + v is scaled at chunk F(e), exponentiated at F(e)+1, summed at F(e)+2
-    auto F = [](int e) constexpr { return (e * 29) / 32; };
+    auto F = [](int e) constexpr { return (e * 29) / (16 * NH); };
     auto chunk = [&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
       if constexpr (q == 0) {
-        l_prev[0] = l_run[0];
-        l_prev[1] = l_run[1];
+#pragma unroll
+        for (int rh = 0; rh < NH; ++rh) l_prev[rh] = l_run[rh];
       }
       if constexpr (q < 8) {          // mask, then row max steps over elements 2q, 2q+1 of both halves
 #pragma unroll
-        for (int rh = 0; rh < 2; ++rh) {
+        for (int rh = 0; rh < NH; ++rh) {
           if constexpr (decltype(masked)::value) {
             mask_elem(Sc, rh, 2 * q, kb);
             mask_elem(Sc, rh, 2 * q + 1, kb);
@@ -408,16 +420,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       }
       if constexpr (q == 9) {
 #pragma unroll
-        for (int rh = 0; rh < 2; ++rh) {
+        for (int rh = 0; rh < NH; ++rh) {
           mt[rh] = pair_max2(mx[rh]);
           anchor(mt[rh]);
         }
       }
       if constexpr (q == 11) {
 #pragma unroll
-        for (int rh = 0; rh < 2; ++rh) g[rh] = mt[rh] > m_run[rh] + th;
+        for (int rh = 0; rh < NH; ++rh) g[rh] = mt[rh] > m_run[rh] + th;
       }
-      static_for<32>([&](auto ec) __attribute__((always_inline)) {
+      static_for<16 * NH>([&](auto ec) __attribute__((always_inline)) {
         constexpr int e = decltype(ec)::value, rh = e / 16, v = e % 16;
         if constexpr (F(e) == q) Sc[rh][v] = fmaf(Sc[rh][v], c, -mc[rh]);
         if constexpr (F(e) + 1 == q) Sc[rh][v] = fast_exp2(Sc[rh][v]);
@@ -433,13 +445,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       });
       if constexpr (q == 31) {
 #pragma unroll
-        for (int rh = 0; rh < 2; ++rh) {
+        for (int rh = 0; rh < NH; ++rh) {
           l_run[rh] += ps[rh][0] + ps[rh][1];
           anchor(l_run[rh]);
         }
       }
     };
-    static_assert(F(31) + 2 <= 31, "softmax schedule");
+    static_assert(F(16 * NH - 1) + 2 <= 31, "softmax schedule");
     bf16x8 kf[KS], vf[NPV];
     auto load_k = [&](int s) __attribute__((always_inline)) { kf[s] = as_bf(ld16(Kn + koff[s & 1] + (s >> 1) * 1024)); };
     auto load_v = [&](int u) __attribute__((always_inline)) {   // u = DB * t2 + mb
@@ -462,18 +474,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     };
 #pragma unroll
     for (int f = 0; f < PF; ++f) load_frag(f);
-    constexpr int NSLOT = 2 * KS + 2 * NPV;
+    constexpr int NSLOT = NH * KS + NH * NPV;
     auto slot = [&](auto ic) __attribute__((always_inline)) {
       constexpr int i = decltype(ic)::value;
-      constexpr int iq = PVF ? (i >= 2 * NPV ? i - 2 * NPV : -1) : (i < 2 * KS ? i : -1);   // score slot index
-      constexpr int ip = PVF ? (i < 2 * NPV ? i : -1) : (i >= 2 * KS ? i - 2 * KS : -1);    // PV slot index
+      constexpr int iq = PVF ? (i >= NH * NPV ? i - NH * NPV : -1) : (i < NH * KS ? i : -1);   // score slot index
+      constexpr int ip = PVF ? (i < NH * NPV ? i : -1) : (i >= NH * KS ? i - NH * KS : -1);    // PV slot index
       if constexpr (iq >= 0) {
-        constexpr int s = iq / 2, rh = iq % 2;
+        constexpr int s = iq / NH, rh = iq % NH;
         if constexpr (rh == 0) load_frag((PVF ? NPV : 0) + s + PF);
         if constexpr (s == 0) mma_v_first(Sn[rh], kf[s], qreg[rh][s]);
         else mma_v(Sn[rh], kf[s], qreg[rh][s]);
       } else {
-        constexpr int u = ip / 2, rh = ip % 2;
+        constexpr int u = ip / NH, rh = ip % NH;
         constexpr int t2 = u / DB, mb = u % DB;
         if constexpr (rh == 0) load_frag((PVF ? 0 : KS) + u + PF);
         mma_a(oacc[rh][mb], vf[u], Pp[rh][t2]);
@@ -486,14 +498,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       sched_fence();
     };
     static_for<NSLOT>(slot);
-    if (__any(g[0] || g[1])) {
+    bool gany = g[0];
+#pragma unroll
+    for (int rh = 1; rh < NH; ++rh) gany = gany || g[rh];
+    if (__any(gany)) {
       // slow path: new row maxima.  Recompute block j's scores (its K rows are still resident),
       // exponentiate them against the new maxima, and rescale O and the running sums.
-      f32x16 R[2];
+      f32x16 R[NH];
       scores(Kc, R);
       mfma_fence();
 #pragma unroll
-      for (int rh = 0; rh < 2; ++rh) {
+      for (int rh = 0; rh < NH; ++rh) {
         pin_v(R[rh]);
         const float m_new = g[rh] ? mt[rh] : m_run[rh];
         const float alpha = (g[rh] && m_run[rh] != kNegInf) ? fast_exp2((m_run[rh] - m_new) * c) : 1.f;
@@ -524,13 +539,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   wait_vmem<CPW * (NS - 2)>();
   __syncthreads();
 
-  f32x16 SA[2], SB[2];
-  bf16x8 PA[2][2], PB[2][2];
+  f32x16 SA[NH], SB[NH];
+  bf16x8 PA[NH][2], PB[NH][2];
   // block 0's scores; block -1's probabilities are zero (its PV products, on tile 0's V rows,
   // add nothing)
   scores(&smem[0][0][0], SA);
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh)
+  for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) PB[rh][t2] = bf16x8{};
   mfma_fence();
@@ -574,18 +589,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       const int t2 = u / DB, mb = u % DB;
       const int o = 16 * t2 * RB + 1024 * mb;
       const bf16x8 v = as_bf(lds_tr(Vl + voff[0] + o), lds_tr(Vl + voff[1] + o));
-      mma_a(oacc[0][mb], v, PB[0][t2]);
-      mma_a(oacc[1][mb], v, PB[1][t2]);
+#pragma unroll
+      for (int rh = 0; rh < NH; ++rh) mma_a(oacc[rh][mb], v, PB[rh][t2]);
     }
     mfma_fence();
 #pragma unroll
-    for (int rh = 0; rh < 2; ++rh)
+    for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
       for (int mb = 0; mb < DB; ++mb) pin_a(oacc[rh][mb]);
   }
 
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh) {
+  for (int rh = 0; rh < NH; ++rh) {
     const float l_tot = pair_sum(l_run[rh]);
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     const float lse = l_tot > 0.f ? m_run[rh] * a.s.scale + logf(l_tot) : kNegInf;
@@ -749,11 +764,11 @@ hipError_t launch_fwd_main(const FwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_items);
   if (bf16) {
     const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
-    if (a.s.rw % 2 == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
+    if (a.s.rw % PSATTN_FWD_NH == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
         a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 4 waves of 64 rows
-      const dim3 block(4 * 64);
-      if (a.s.d == 128) hipLaunchKernelGGL((fwd_bf16_w64_kernel<128, 4, PSATTN_FWD_NS>), grid, block, 0, st, a);
-      else hipLaunchKernelGGL((fwd_bf16_w64_kernel<64, 4, PSATTN_FWD_NS>), grid, block, 0, st, a);
+      const dim3 block(8 / PSATTN_FWD_NH * 64);
+      if (a.s.d == 128) hipLaunchKernelGGL((fwd_bf16_w64_kernel<128, 8 / PSATTN_FWD_NH, PSATTN_FWD_NS, PSATTN_FWD_NH>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((fwd_bf16_w64_kernel<64, 8 / PSATTN_FWD_NH, PSATTN_FWD_NS, PSATTN_FWD_NH>), grid, block, 0, st, a);
       return hipGetLastError();
     }
     const dim3 block(a.s.nw * 64);
