@@ -16,8 +16,14 @@
 
 #include "psattn_device.h"
 
+// 32-row halves per wavefront of the bf16 dQ kernel: 2 (one wavefront per SIMD) or 1 (two; with
+// Q, dO and dQ in 128 AGPRs it has 128 VGPRs for the rest and measured 1-3% slower on c2)
+#ifndef PSATTN_DQ_NH
+#define PSATTN_DQ_NH 2
+#endif
+// fragment prefetch distance of the dQ kernel (3 keeps the two-wavefront form within 128 VGPRs)
 #ifndef PSATTN_DQ_PF
-#define PSATTN_DQ_PF 4
+#define PSATTN_DQ_PF (PSATTN_DQ_NH == 1 ? 3 : 4)
 #endif
 
 namespace psattn {
@@ -885,13 +891,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 }
 
 // ============================================================================================
-// bf16 dQ kernel, 64 rows per wavefront (the structure of the forward 64-row kernel).  One
-// wavefront per SIMD holds Q, dO and the dQ accumulators of 64 rows of one head in AGPRs and the
-// scores in VGPRs.  Stage j issues the S = K Q^T and dP = V dO^T MFMAs of 32-key block j+1 and
-// the dQ^T += K^T dS^T MFMAs of block j-1, and between them computes P = exp2(S c - LSE log2 e)
-// and dS = P (dP - Delta) of block j.  Every K or V fragment read from LDS feeds two MFMAs.
-template <int D, int NW, int NS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1))) void bwd_dq_bf16_w64_kernel(BwdArgs a) {
+// bf16 dQ kernel (the structure of the forward kernel).  A wavefront holds Q, dO and the dQ
+// accumulators of NH 32-row halves of one head in AGPRs and the scores in VGPRs; with NH = 2,
+// one wavefront per SIMD, and every K or V fragment read from LDS feeds two MFMAs.  Stage j
+// issues the S = K Q^T and dP = V dO^T MFMAs of 32-key block j+1 and the dQ^T += K^T dS^T MFMAs
+// of block j-1, and between them computes P = exp2(S c - LSE log2 e) and dS = P (dP - Delta) of
+// block j.
+template <int D, int NW, int NS, int NH>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH, 3 - NH))) void bwd_dq_bf16_w64_kernel(BwdArgs a) {
   constexpr int RB = D * 2;
   constexpr int CPR = D / 8;
   constexpr int RPI = 64 / CPR;
@@ -912,8 +919,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int rw2 = a.s.rw >> 1;
-  const int head = it.head0 + wave / rw2;
+  const int rwn = a.s.rw / NH;                   // NH*32-row blocks per head
+  const int head = it.head0 + wave / rwn;
   const int hk = it.head0 / a.s.g;
   const int nkv = it.nkv;
   const int* kvl = a.plan.kv_list + it.kv_off;
@@ -924,13 +931,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     if (nkv > IDX_BLK) s_slot[1][i] = kvl[min(IDX_BLK + i, nkv - 1)];
   }
 
-  int ridx[2], row[2], lim[2];
-  bool row_ok[2];
-  float lse2[2], del[2];
-  bf16x8 qreg[2][KS], doreg[2][KS];
+  int ridx[NH], row[NH], lim[NH];
+  bool row_ok[NH];
+  float lse2[NH], del[NH];
+  bf16x8 qreg[NH][KS], doreg[NH][KS];
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh) {
-    ridx[rh] = (wave % rw2) * 64 + 32 * rh + l32;
+  for (int rh = 0; rh < NH; ++rh) {
+    ridx[rh] = (wave % rwn) * (32 * NH) + 32 * rh + l32;
     row_ok[rh] = ridx[rh] < it.nq;
     row[rh] = a.plan.q_list[it.q_off + (row_ok[rh] ? ridx[rh] : it.nq - 1)];
     lim[rh] = min(nkv - 1, a.plan.row_pos[row[rh]] - it.kv_pos0);
@@ -955,17 +962,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 #pragma unroll
     for (int rd = 0; rd < 2; ++rd) toff[rd] = gtile_off<D>(8 * rd + 4 * hh + r4, (dsub + 4 * j) >> 3) + 8 * (j & 1);
   }
-  static_assert(NW == 4 && IPW == D / 32, "copies: wave w fills row group w of a tile, IPW units per tensor");
+  static_assert(NW * NH == 8 && IPW * NW == CPR, "copies: NW / 4 waves per row group of a tile, IPW units each");
 
   const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
   const uint8_t* Kb = (const uint8_t*)a.K + (size_t)hk * D * sizeof(bf16_t);
   const uint8_t* Vb = (const uint8_t*)a.V + (size_t)hk * D * sizeof(bf16_t);
-  // Copies: wave w fills row group w (keys 16 w .. 16 w + 15) of every tile, one 1 KB unit
-  // (chunks 4 i .. 4 i + 3) per instruction i.  Lane l writes chunk 4 i + l / 16 of the row at
-  // position l % 16, i.e. of key row (l % 16) ^ 4 (l / 16) of the group.
-  const int crow = 16 * wave + ((lane & 15) ^ (4 * (lane >> 4)));
-  const uint32_t cbyte = (uint32_t)(lane >> 4) << 4;
-  const uint32_t smem_base = lds_addr(&smem[0][0][0]) + wave * 16 * RB;
+  // Copies: row group cg = wave / (NW/4) (keys 16 cg .. 16 cg + 15) of every tile is filled by
+  // NW/4 waves, wave w taking the IPW 1 KB units u0 + i, u0 = IPW (w mod NW/4), one per
+  // instruction i (unit u holds chunks 4u .. 4u + 3).  Lane l writes chunk 4u + l / 16 of the
+  // row at position l % 16, i.e. of key row (l % 16) ^ 4 (l / 16) of the group.
+  const int cg = wave / (NW / 4), u0 = (wave % (NW / 4)) * IPW;
+  const int crow = 16 * cg + ((lane & 15) ^ (4 * (lane >> 4)));
+  const uint32_t cbyte = ((uint32_t)(lane >> 4) << 4) + 64 * u0;
+  const uint32_t smem_base = lds_addr(&smem[0][0][0]) + cg * 16 * RB + u0 * 1024;
   // the slot of this lane's copy row in key tile t (the two staged index blocks are contiguous:
   // entry key sits at key mod 2*IDX_BLK)
   auto issue_slot = [&](int t) __attribute__((always_inline)) {
@@ -993,16 +1002,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
   };
 
-  f32x16 dq[2][DB];
+  f32x16 dq[NH][DB];
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh)
+  for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
     for (int mb = 0; mb < DB; ++mb) {
       dq[rh][mb] = f32x16{};
       pin_a(dq[rh][mb]);
     }
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh)
+  for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       pin_a(qreg[rh][s]);
@@ -1011,21 +1020,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   valu_fence();
   const float c = a.s.scale * kLog2e;
 
-  auto mask_elem = [&](f32x16 (&S)[2], int rh, int v, int kb) __attribute__((always_inline)) {
+  auto mask_elem = [&](f32x16 (&S)[NH], int rh, int v, int kb) __attribute__((always_inline)) {
     const int x = lim[rh] - kb - 4 * hh;    // element v holds key kb + 4*hh + 8*(v/4) + v%4
     S[rh][v] = (8 * (v >> 2) + (v & 3) > x) ? kNegInf : S[rh][v];
   };
   // ---- one stage.  Sc, dPc: block j (dS now); Sn, dPn: block j+1 (MFMAs now, K and V rows at
   // Kn, Vn); dSp: dS of block j-1 (dQ MFMAs now, K rows at Kp); dSc: block j's dS (written).
-  auto stage = [&](f32x16 (&Sc)[2], f32x16 (&dPc)[2], f32x16 (&Sn)[2], f32x16 (&dPn)[2],
-                   const bf16x8 (&dSp)[2][2], bf16x8 (&dSc)[2][2], const uint8_t* Kn, const uint8_t* Vn,
+  auto stage = [&](f32x16 (&Sc)[NH], f32x16 (&dPc)[NH], f32x16 (&Sn)[NH], f32x16 (&dPn)[NH],
+                   const bf16x8 (&dSp)[NH][2], bf16x8 (&dSc)[NH][2], const uint8_t* Kn, const uint8_t* Vn,
                    const uint8_t* Kp, int kb, auto masked, auto extra, auto dq_first) __attribute__((always_inline)) {
     // element e = 16 rh + v: scaled and shifted at chunk F(e), exponentiated at F(e)+1,
     // multiplied by dP - Delta at F(e)+2; each 8-element group is packed after its last product
-    auto F = [](int e) constexpr { return (e * 29) / 32; };
+    auto F = [](int e) constexpr { return (e * 29) / (16 * NH); };
     auto chunk = [&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
-      static_for<32>([&](auto ec) __attribute__((always_inline)) {
+      static_for<16 * NH>([&](auto ec) __attribute__((always_inline)) {
         constexpr int e = decltype(ec)::value, rh = e / 16, v = e % 16;
         if constexpr (F(e) == q) {
           if constexpr (decltype(masked)::value) mask_elem(Sc, rh, v, kb);
@@ -1040,7 +1049,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
         }
       });
     };
-    static_assert(F(31) + 2 <= 31, "dS schedule");
+    static_assert(F(16 * NH - 1) + 2 <= 31, "dS schedule");
     bf16x8 kf[KS], vf[KS], tf[NDQ];
     auto load_k = [&](int s) __attribute__((always_inline)) {
       kf[s] = as_bf(ld16(Kn + koff[s & 1] + (s >> 1) * 1024));
@@ -1066,15 +1075,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     };
 #pragma unroll
     for (int f = 0; f < PF; ++f) load_frag(f);
-    constexpr int NS_SLOTS = 4 * KS, NQ_SLOTS = 2 * NDQ, NSLOT = NS_SLOTS + NQ_SLOTS;
+    constexpr int NS_SLOTS = 2 * NH * KS, NQ_SLOTS = NH * NDQ, NSLOT = NS_SLOTS + NQ_SLOTS;
     auto slot = [&](auto ic) __attribute__((always_inline)) {
       constexpr int i = decltype(ic)::value;
       constexpr int is = DQF ? (i >= NQ_SLOTS ? i - NQ_SLOTS : -1) : (i < NS_SLOTS ? i : -1);   // S/dP slot
       constexpr int iq = DQF ? (i < NQ_SLOTS ? i : -1) : (i >= NS_SLOTS ? i - NS_SLOTS : -1);   // dQ slot
       if constexpr (is >= 0) {
-        constexpr int s = is / 4, w = is % 4, rh = w & 1;
+        constexpr int s = is / (2 * NH), w = is % (2 * NH), rh = w % NH;   // w < NH: S, else dP
         if constexpr (w == 0) load_frag((DQF ? NDQ : 0) + s + PF);
-        if constexpr (w < 2) {
+        if constexpr (w < NH) {
           if constexpr (s == 0) mma_v_first(Sn[rh], kf[s], qreg[rh][s]);
           else mma_v(Sn[rh], kf[s], qreg[rh][s]);
         } else {
@@ -1082,7 +1091,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
           else mma_v(dPn[rh], vf[s], doreg[rh][s]);
         }
       } else {
-        constexpr int u = iq / 2, rh = iq % 2;
+        constexpr int u = iq / NH, rh = iq % NH;
         constexpr int t2 = u / DB, mb = u % DB;
         if constexpr (rh == 0) load_frag((DQF ? 0 : KS) + u + PF);
         mma_a(dq[rh][mb], tf[u], dSp[rh][t2]);
@@ -1103,8 +1112,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
   wait_vmem<CPW * (NS - 2)>();
   __syncthreads();
 
-  f32x16 SA[2], SB[2], dPA[2], dPB[2];
-  bf16x8 dSA[2][2], dSB[2][2];
+  f32x16 SA[NH], SB[NH], dPA[NH], dPB[NH];
+  bf16x8 dSA[NH][2], dSB[NH][2];
   // block 0's S and dP; block -1's dS is zero (its dQ products, on tile 0's K rows, add nothing)
   {
     const uint8_t* K0 = &smem[0][0][0];
@@ -1114,7 +1123,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       const bf16x8 k = as_bf(ld16(K0 + koff[s & 1] + (s >> 1) * 1024));
       const bf16x8 v = as_bf(ld16(V0 + koff[s & 1] + (s >> 1) * 1024));
 #pragma unroll
-      for (int rh = 0; rh < 2; ++rh) {
+      for (int rh = 0; rh < NH; ++rh) {
         if (s == 0) {
           mma_v_first(SA[rh], k, qreg[rh][s]);
           mma_v_first(dPA[rh], v, doreg[rh][s]);
@@ -1125,7 +1134,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       }
     }
 #pragma unroll
-    for (int rh = 0; rh < 2; ++rh)
+    for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2) dSB[rh][t2] = bf16x8{};
     mfma_fence();
@@ -1172,19 +1181,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
       const int t2 = u / DB, mb = u % DB;
       const int o = 16 * t2 * RB + 1024 * mb;
       const bf16x8 k = as_bf(lds_tr(Kl + toff[0] + o), lds_tr(Kl + toff[1] + o));
-      mma_a(dq[0][mb], k, dSB[0][t2]);
-      mma_a(dq[1][mb], k, dSB[1][t2]);
+#pragma unroll
+      for (int rh = 0; rh < NH; ++rh) mma_a(dq[rh][mb], k, dSB[rh][t2]);
     }
     mfma_fence();
 #pragma unroll
-    for (int rh = 0; rh < 2; ++rh)
+    for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
       for (int mb = 0; mb < DB; ++mb) pin_a(dq[rh][mb]);
   }
 
   const float scale = a.s.scale;
 #pragma unroll
-  for (int rh = 0; rh < 2; ++rh) {
+  for (int rh = 0; rh < NH; ++rh) {
     if (!row_ok[rh]) continue;
     float* dst = it.part < 0 ? a.dQ + ((size_t)row[rh] * a.s.hq + head) * D
                              : a.part_dq + (((size_t)it.part + ridx[rh]) * a.s.hq + head) * D;
@@ -1481,11 +1490,12 @@ hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_fwd);
   if (bf16) {
     const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
-    if (a.s.rw % 2 == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
-        a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 4 waves of 64 rows
-      const dim3 block(4 * 64);
-      if (a.s.d == 128) hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<128, 4, 4>), grid, block, 0, st, a);
-      else hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<64, 4, 4>), grid, block, 0, st, a);
+    if (a.s.rw % PSATTN_DQ_NH == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
+        a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 8 / NH waves of NH*32 rows
+      constexpr int NW = 8 / PSATTN_DQ_NH;
+      const dim3 block(NW * 64);
+      if (a.s.d == 128) hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<128, NW, 4, PSATTN_DQ_NH>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<64, NW, 4, PSATTN_DQ_NH>), grid, block, 0, st, a);
       return hipGetLastError();
     }
     const dim3 block(a.s.nw * 64);
