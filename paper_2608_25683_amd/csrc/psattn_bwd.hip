@@ -1361,40 +1361,71 @@ __global__ __launch_bounds__(512) void bwd_dq_f32_kernel(BwdArgs a) {
 
 // ============================================================================================
 // Delta = rowsum(dO * O) per (row, head), and LSE * log2(e) for the exp2-based kernels;
-// D/8 lanes per (row, head), 8 elements each
+// D/8 lanes per (row, head), 8 elements each.  A workgroup takes PRE_PASSES x (256 / (D/8))
+// consecutive rows of one head, so the per-head statistics ([head][row]) are written as
+// contiguous runs; every lane issues all its loads before the first product.
+constexpr int PRE_PASSES = 4;
 template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
-  const int D = a.s.d, hq = a.s.hq;
+  const int D = a.s.d, hq = a.s.hq, ns = a.s.ns;
   const int lanes = D / 8;
-  const int per_block = 256 / lanes;
-  const int rh = blockIdx.x * per_block + threadIdx.x / lanes;
+  const int per_pass = 256 / lanes;
+  const int blocks_per_head = (ns + per_pass * PRE_PASSES - 1) / (per_pass * PRE_PASSES);
+  const int h = blockIdx.x / blocks_per_head;
+  const int row0 = (blockIdx.x % blocks_per_head) * per_pass * PRE_PASSES + threadIdx.x / lanes;
   const int sub = threadIdx.x % lanes;
-  const bool ok = rh < a.s.ns * hq;
-  float acc = 0.f;
-  if (ok) {
-    const size_t o = (size_t)rh * D + sub * 8;
-    if (BF16) {
-      const u32x4 x = ld16((const bf16_t*)a.O + o), y = ld16((const bf16_t*)a.dO + o);
+  float acc[PRE_PASSES];
+  if (BF16) {
+    u32x4 x[PRE_PASSES], y[PRE_PASSES];
+#pragma unroll
+    for (int p = 0; p < PRE_PASSES; ++p) {
+      const int row = min(row0 + p * per_pass, ns - 1);
+      const size_t o = ((size_t)row * hq + h) * D + sub * 8;
+      x[p] = ld16((const bf16_t*)a.O + o);
+      y[p] = ld16((const bf16_t*)a.dO + o);
+    }
+#pragma unroll
+    for (int p = 0; p < PRE_PASSES; ++p) {
+      acc[p] = 0.f;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        acc = fmaf(bf2f(x[e] & 0xffffu), bf2f(y[e] & 0xffffu), acc);
-        acc = fmaf(bf2f(x[e] >> 16), bf2f(y[e] >> 16), acc);
+        acc[p] = fmaf(bf2f(x[p][e] & 0xffffu), bf2f(y[p][e] & 0xffffu), acc[p]);
+        acc[p] = fmaf(bf2f(x[p][e] >> 16), bf2f(y[p][e] >> 16), acc[p]);
       }
-    } else {
-      const float* x = (const float*)a.O + o;
-      const float* y = (const float*)a.dO + o;
+    }
+  } else {
+    f32x4 x[PRE_PASSES][2], y[PRE_PASSES][2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc = fmaf(x[e], y[e], acc);
+    for (int p = 0; p < PRE_PASSES; ++p) {
+      const int row = min(row0 + p * per_pass, ns - 1);
+      const size_t o = ((size_t)row * hq + h) * D + sub * 8;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        x[p][k] = *(const f32x4*)((const float*)a.O + o + 4 * k);
+        y[p][k] = *(const f32x4*)((const float*)a.dO + o + 4 * k);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < PRE_PASSES; ++p) {
+      acc[p] = 0.f;
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[p] = fmaf(x[p][k][e], y[p][k][e], acc[p]);
     }
   }
-  for (int w = lanes / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
-  if (ok && sub == 0) {
-    const int row = rh / hq, h = rh % hq;
-    const size_t o = (size_t)h * a.s.ns + row;
-    a.delta[o] = acc;
-    a.lse2[o] = a.LSE[o] * kLog2e;
-    ((uint32_t*)a.kv_nls)[o] = split_bf16(-a.LSE[o] / a.s.scale);
-    ((uint32_t*)a.kv_nd)[o] = split_bf16(-acc);
+#pragma unroll
+  for (int p = 0; p < PRE_PASSES; ++p) {
+    for (int w = lanes / 2; w >= 1; w >>= 1) acc[p] += __shfl_xor(acc[p], w);
+    const int row = row0 + p * per_pass;
+    if (row < ns && sub == 0) {
+      const size_t o = (size_t)h * ns + row;
+      const float lse = a.LSE[o];
+      a.delta[o] = acc[p];
+      a.lse2[o] = lse * kLog2e;
+      ((uint32_t*)a.kv_nls)[o] = split_bf16(-lse / a.s.scale);
+      ((uint32_t*)a.kv_nd)[o] = split_bf16(-acc[p]);
+    }
   }
 }
 
@@ -1457,9 +1488,9 @@ __global__ __launch_bounds__(256) void bwd_zero_pad_kernel(BwdArgs a) {
   }
 
 hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st) {
-  const int per_block = 256 / (a.s.d / 8);
-  const int64_t n = (int64_t)a.s.ns * a.s.hq;
-  const dim3 grid((unsigned)((n + per_block - 1) / per_block));
+  const int rows_per_block = 256 / (a.s.d / 8) * PRE_PASSES;
+  const int64_t blocks_per_head = ((int64_t)a.s.ns + rows_per_block - 1) / rows_per_block;
+  const dim3 grid((unsigned)(blocks_per_head * a.s.hq));
   if (bf16) hipLaunchKernelGGL((bwd_pre_kernel<true>), grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL((bwd_pre_kernel<false>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
