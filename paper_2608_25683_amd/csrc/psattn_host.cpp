@@ -227,12 +227,12 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   s.hkv = t->hkv;
   s.d = t->d;
   s.g = t->hq / t->hkv;
-  s.hc = 1;
-  for (int c = 8; c >= 1; --c)
-    if (s.g % c == 0) { s.hc = c; break; }
-  // 32-row subtiles per head: a forward/dQ workgroup holds up to 8 wavefronts (hc x rw), so
-  // each staged key tile serves up to 8 x 32 query-head rows
-  s.rw = (8 % s.hc == 0) ? 8 / s.hc : (s.hc <= 4 ? 2 : 1);
+  // Heads per forward/dQ item: the largest common divisor of G and 4, and 32-row subtiles per
+  // head rw = 8 / hc (2, 4 or 8).  Every item is then 8 subtile x head pairs, which the
+  // eight-wavefront kernels need, and each staged key tile serves 8 x 32 query-head rows.  (For
+  // G = 5 or 7 that means one head per item with 256-row query tiles.)
+  s.hc = s.g % 4 == 0 ? 4 : (s.g % 2 == 0 ? 2 : 1);
+  s.rw = 8 / s.hc;
   s.nw = s.hc * s.rw;
   s.bmq = Q_SUB * s.rw;
   s.scale = t->scale;

@@ -257,13 +257,15 @@ def test_forced_splits_produce_partials():
     _check_plan(wl, t)
 
 
-@pytest.mark.parametrize("hq,hkv", [(4, 4), (6, 2), (10, 2), (16, 1), (12, 4)])
+@pytest.mark.parametrize("hq,hkv", [(4, 4), (6, 2), (10, 2), (16, 1), (12, 4), (40, 8), (14, 2)])
 def test_plan_head_chunks(hq, hkv):
     wl = W.random_forest(7, max_nodes=6, max_seg=70, hq=hq, hkv=hkv, tensors=False)
     t = P.Tree.from_workload(wl)
     G = hq // hkv
     hc = t.info["head_chunk"]
-    assert G % hc == 0 and hc <= 8
+    # the largest common divisor of G and 4; every item holds 8 (32-row subtile, head) pairs
+    assert hc == max(c for c in (1, 2, 4) if G % c == 0)
+    assert t.info["q_tile_rows"] * hc == 8 * 32
     _check_plan(wl, t)
 
 
