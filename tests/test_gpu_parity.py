@@ -81,6 +81,33 @@ def test_scaled_down_workloads(name):
     H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
 
 
+# degenerate trees: one-token nodes, many tiny siblings, a deep chain of one-token nodes, a
+# one-token root under a long child, many single-token roots
+DEGENERATE = {
+    "one_token": dict(parent=[-1], seg=[1], samples=[0], hq=4, hkv=2, d=128, dtype="bf16"),
+    # (G = 1: the root key's dV sums 41 terms with P near 1/2; its error from the bf16 P of the dV
+    # product grows with the square root of that count, see the tolerance reading)
+    "tiny_siblings": dict(parent=[-1] + [0] * 40, seg=[1] * 41, samples=list(range(1, 41)), hq=2, hkv=2, d=128,
+                          dtype="bf16"),
+    "token_chain": dict(parent=[-1] + list(range(69)), seg=[1] * 70, samples=[69, 30], hq=8, hkv=2, d=64,
+                        dtype="bf16"),
+    "short_root_long_child": dict(parent=[-1, 0], seg=[1, 700], samples=[1], hq=8, hkv=2, d=128, dtype="bf16"),
+    "single_token_roots": dict(parent=[-1] * 33, seg=[1] * 33, samples=list(range(33)), hq=4, hkv=4, d=64,
+                               dtype="bf16"),
+    "token_chain_fp32": dict(parent=[-1] + list(range(39)), seg=[1] * 40, samples=[39], hq=4, hkv=2, d=64,
+                             dtype="fp32"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DEGENERATE))
+def test_degenerate_trees(name):
+    c = DEGENERATE[name]
+    wl = W.custom(c["parent"], c["seg"], c["samples"], hq=c["hq"], hkv=c["hkv"], d=c["d"], dtype=c["dtype"], seed=11,
+                  sigma=1.0 if c["dtype"] == "fp32" else 0.5, block_policy=W.blocks_exact)
+    _say(f"degenerate {name} rows={wl.tree.num_rows}")
+    H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+
+
 # --------------------------------------------------------------------------- robustness and determinism
 
 def test_bitwise_repeatable():
