@@ -2,22 +2,27 @@
 // fixed-order reductions of split partial results, and zeroing of pool slots holding no token.
 //
 // bf16 dK/dV kernel (gfx950).  One workgroup = one BkvItem: up to 128 keys of one node and one
-// kv head (wave w keeps keys 32w..32w+31 of K and V in registers) x a chunk of the rows that
-// consume them -- the node's own later rows and every row of every descendant node, i.e. all
-// branches reusing the prefix.  For each 32-row subtile and each query head of the group it
-// computes S = Q K^T and dP = dO V^T (lane <-> key), P = exp(S*scale - LSE), dS = P*(dP - Delta),
-// then dV += P^T dO and dK += dS^T Q, whose B operands (dO^T, Q^T) come from transposing LDS
-// reads of the row-major tiles.  Q/dO tiles and the LSE/Delta rows are copied global -> LDS
-// directly into a two-stage ring.  Consumer-row indices are staged in LDS 256 at a time.
+// kv head x a chunk of the rows that consume them -- the node's own later rows and every row of
+// every descendant node, i.e. all branches reusing the prefix.  For each 32-row subtile and each
+// query head of the group it computes S = Q K^T and dP = dO V^T (lane <-> key),
+// P = exp(S*scale - LSE), dS = P*(dP - Delta), then dV += P^T dO and dK += dS^T Q, whose B
+// operands (dO^T, Q^T) come from transposing LDS reads of the row-major tiles.  The main form
+// (bwd_kv_bf16_1w_kernel) runs one wavefront per SIMD, wave w keeping keys 32w..32w+31 of K and
+// V and their dK/dV accumulators in registers, and streams Q/dO rows and the LSE/Delta values
+// global -> LDS directly into a five-step ring; the older eight-wavefront form (bwd_kv_bf16_kernel)
+// remains for pools and tensors beyond 32-bit byte offsets.  Consumer-row indices are staged in
+// LDS 256 at a time.
 //
-// bf16 dQ kernel: same items and wave layout as the forward kernel; recomputes S^T and dP^T per
-// key tile and accumulates dQ^T += K^T dS^T, K^T again from transposing reads.
+// bf16 dQ kernel: the same items as the forward kernel and its structure (NH 32-row halves per
+// wave); recomputes S^T and dP^T per key tile and accumulates dQ^T += K^T dS^T, K^T again from
+// transposing reads.
 #include <algorithm>
 
 #include "psattn_device.h"
 
 // 32-row halves per wavefront of the bf16 dQ kernel: 2 (one wavefront per SIMD) or 1 (two; with
-// Q, dO and dQ in 128 AGPRs it has 128 VGPRs for the rest and measured 1-3% slower on c2)
+// Q, dO and dQ in 128 AGPRs it has 128 VGPRs for the rest, and measured 1-3% slower on a
+// 32q/8kv-head, d = 128 tree of a 4096-token prefix and 16 branches of 1024)
 #ifndef PSATTN_DQ_NH
 #define PSATTN_DQ_NH 2
 #endif

@@ -1,17 +1,19 @@
 // Forward kernels: bf16 MFMA main kernel, fp32 VALU kernel, log-sum-exp merge of split pieces.
 //
-// bf16 main kernel (gfx950).  One workgroup = one FwdItem: up to 32*rw query rows x hc query
-// heads (all reading one kv head) x a range of keys along the node's root-to-node path.  Wave w
-// owns head head0 + w / rw and 32 rows; it computes the transposed score tile S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16, so each lane holds one query row: softmax statistics are per-lane
-// scalars and one v_permlane32_swap completes each row reduction.  The probabilities leave the
-// accumulators as the B operand of O^T += V^T P^T without any data movement; V^T comes from a
-// transposing LDS read (ds_read_b64_tr_b16) of the row-major V tile.
+// bf16 kernels (gfx950).  One workgroup = one FwdItem: 32*rw query rows x hc query heads (all
+// reading one kv head) x a range of keys along the node's root-to-node path.  A wave computes the
+// transposed score tile S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane holds one query
+// row: softmax statistics are per-lane scalars and one v_permlane32_swap completes each row
+// reduction.  The probabilities leave the accumulators as the B operand of O^T += V^T P^T without
+// any data movement; V^T comes from a transposing LDS read (ds_read_b64_tr_b16).
 //
-// Key tiles (64 keys) are gathered through the path's slot list, one 256-byte row per key and
-// head, and copied global -> LDS directly (global_load_lds_dwordx4) into a two-stage ring; the
-// copies for tile t+1 run while tile t is computed.  The running max is only moved when it grows
-// by more than 2^8, so O and the row sum are rarely rescaled.
+// Key tiles (64 keys) are gathered through the path's slot list, one row per key, and copied
+// global -> LDS directly (global_load_lds_dwordx4) into a ring while earlier tiles are computed:
+// a 4-stage ring in the grouped layout of gtile_off for the main kernel (fwd_bf16_w64_kernel,
+// NH 32-row halves per wave), a 2-stage ring of swizzled rows for the older multi-wave kernel
+// (fwd_bf16_kernel, one 32-row subtile per wave; used where the main kernel's 32-bit offsets
+// do not reach).  The running max is only moved when it grows by more than 2^8, so O and the
+// row sum are rarely rescaled.
 #include "psattn_device.h"
 
 #ifndef PSATTN_FWD_NS
