@@ -956,6 +956,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
     }
   }
 
+  // dP accumulators start at -Delta: one MFMA of A = 1 on k = 0, 1 (every key) and B = the (hi, lo)
+  // bf16 split of the column's -Delta on k = 0, 1 (zero on lanes 32-63, which hold k = 8..15)
+  const bf16x8 ones_k01 = as_bf(hh ? u32x4{0u, 0u, 0u, 0u} : u32x4{0x3F803F80u, 0u, 0u, 0u});
+  bf16x8 ndel[NH];
+#pragma unroll
+  for (int rh = 0; rh < NH; ++rh) ndel[rh] = as_bf(u32x4{hh ? 0u : split_bf16(-del[rh]), 0u, 0u, 0u});
   // LDS byte offsets of this lane's fragments inside a 32-key block (gtile_off layout): K or V
   // fragment s (rows l32, chunk 2s + hh) at koff[s & 1] + 1024 (s >> 1); K^T fragment of k-step
   // t2 and d block mb (rows 16 t2 + 8 rd + 4 hh + r4, chunks 4 mb + (dsub + 4 j) / 8) at
@@ -1044,7 +1050,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
         if constexpr (F(e) == q) {
           if constexpr (decltype(masked)::value) mask_elem(Sc, rh, v, kb);
           Sc[rh][v] = fmaf(Sc[rh][v], c, -lse2[rh]);
-          dPc[rh][v] = dPc[rh][v] - del[rh];
         }
         if constexpr (F(e) + 1 == q) Sc[rh][v] = fast_exp2(Sc[rh][v]);
         if constexpr (F(e) + 2 == q) dPc[rh][v] = Sc[rh][v] * dPc[rh][v];
@@ -1080,20 +1085,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
     };
 #pragma unroll
     for (int f = 0; f < PF; ++f) load_frag(f);
-    constexpr int NS_SLOTS = 2 * NH * KS, NQ_SLOTS = NH * NDQ, NSLOT = NS_SLOTS + NQ_SLOTS;
+    constexpr int NS_SLOTS = NH + 2 * NH * KS, NQ_SLOTS = NH * NDQ, NSLOT = NS_SLOTS + NQ_SLOTS;
     auto slot = [&](auto ic) __attribute__((always_inline)) {
       constexpr int i = decltype(ic)::value;
       constexpr int is = DQF ? (i >= NQ_SLOTS ? i - NQ_SLOTS : -1) : (i < NS_SLOTS ? i : -1);   // S/dP slot
       constexpr int iq = DQF ? (i < NQ_SLOTS ? i : -1) : (i >= NS_SLOTS ? i - NS_SLOTS : -1);   // dQ slot
-      if constexpr (is >= 0) {
-        constexpr int s = is / (2 * NH), w = is % (2 * NH), rh = w % NH;   // w < NH: S, else dP
+      if constexpr (is >= 0 && is < NH) {
+        mma_vv_first(dPn[is], ones_k01, ndel[is]);   // dP starts at -Delta
+      } else if constexpr (is >= 0) {
+        constexpr int s = (is - NH) / (2 * NH), w = (is - NH) % (2 * NH), rh = w % NH;   // w < NH: S, else dP
         if constexpr (w == 0) load_frag((DQF ? NDQ : 0) + s + PF);
         if constexpr (w < NH) {
           if constexpr (s == 0) mma_v_first(Sn[rh], kf[s], qreg[rh][s]);
           else mma_v(Sn[rh], kf[s], qreg[rh][s]);
         } else {
-          if constexpr (s == 0) mma_v_first(dPn[rh], vf[s], doreg[rh][s]);
-          else mma_v(dPn[rh], vf[s], doreg[rh][s]);
+          mma_v(dPn[rh], vf[s], doreg[rh][s]);
         }
       } else {
         constexpr int u = iq / NH, rh = iq % NH;
@@ -1131,7 +1137,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
       for (int rh = 0; rh < NH; ++rh) {
         if (s == 0) {
           mma_v_first(SA[rh], k, qreg[rh][s]);
-          mma_v_first(dPA[rh], v, doreg[rh][s]);
+          mma_vv_first(dPA[rh], ones_k01, ndel[rh]);
+          mma_v(dPA[rh], v, doreg[rh][s]);
         } else {
           mma_v(SA[rh], k, qreg[rh][s]);
           mma_v(dPA[rh], v, doreg[rh][s]);
@@ -1177,6 +1184,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
   int t = 0;
   for (; t < min(it.nfull, ntiles); ++t) tile(t, Flag<false>{});
   for (; t < ntiles; ++t) tile(t, Flag<true>{});
+  // the last stage's S and dP MFMAs (of the block past the end) have no readers: their registers
+  // may be reused at once, so let them finish first (scheduling barriers keep the epilogue's
+  // address arithmetic behind the wait states)
+  sched_fence();
+  mfma_fence();
+  sched_fence();
   wait_vmem<0>();   // no copy may still be writing this workgroup's LDS when it ends
   // dQ of the last block
   {

@@ -186,6 +186,10 @@ __device__ __forceinline__ void mma_v_first(f32x16& d, const bf16x8& a, const bf
 __device__ __forceinline__ void mma_v(f32x16& d, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
 }
+// d = a * b, d, a and b in VGPRs
+__device__ __forceinline__ void mma_vv_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "v"(b));
+}
 // d = a * b and d += a * b with d and b in AGPRs
 __device__ __forceinline__ void mma_aa_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&a"(d) : "v"(a), "a"(b));
