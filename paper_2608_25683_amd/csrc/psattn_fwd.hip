@@ -601,14 +601,22 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
       for (int mb = 0; mb < DB; ++mb) pin_a(oacc[rh][mb]);
   }
 
+  // Unsplit items write O as whole rows: each wave stages its normalized bf16 rows in the LDS ring
+  // (free once every wave has finished the PV products above; padded row stride OS), then copies
+  // them out 16 bytes per lane, 1 KB of consecutive row bytes per instruction.  Row index and
+  // validity of staged row r come from lane r % 32 of the half that owns it.
+  constexpr int OS = RB + 16;
+  static_assert(NW * 32 * NH * OS <= NS * 2 * TB, "staged O rows fit the ring");
+  const bool direct = it.part < 0;
+  uint8_t* ot = &smem[0][0][0] + wave * (32 * NH) * OS;
+  if (direct) __syncthreads();
 #pragma unroll
   for (int rh = 0; rh < NH; ++rh) {
     const float l_tot = pair_sum(l_run[rh]);
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     const float lse = l_tot > 0.f ? m_run[rh] * a.s.scale + logf(l_tot) : kNegInf;
-    if (!row_ok[rh]) continue;
-    if (it.part < 0) {
-      bf16_t* op = (bf16_t*)a.O + ((size_t)row[rh] * a.s.hq + head) * D;
+    if (direct) {
+      uint8_t* orow = ot + (32 * rh + l32) * OS;
 #pragma unroll
       for (int mb = 0; mb < DB; ++mb)
 #pragma unroll
@@ -616,10 +624,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
           u32x2 w;
           w[0] = pack2(oacc[rh][mb][4 * g4 + 0] * inv, oacc[rh][mb][4 * g4 + 1] * inv);
           w[1] = pack2(oacc[rh][mb][4 * g4 + 2] * inv, oacc[rh][mb][4 * g4 + 3] * inv);
-          *(u32x2*)(op + 32 * mb + 8 * g4 + 4 * hh) = w;
+          *(u32x2*)(orow + 2 * (32 * mb + 8 * g4 + 4 * hh)) = w;
         }
-      if (hh == 0) a.LSE[(size_t)head * a.s.ns + row[rh]] = lse;
-    } else {
+      if (row_ok[rh] && hh == 0) a.LSE[(size_t)head * a.s.ns + row[rh]] = lse;
+      continue;
+    }
+    if (!row_ok[rh]) continue;
+    {
       const size_t prow = (size_t)it.part + ridx[rh];
       float* op = a.part_o + (prow * a.s.hq + head) * D;
 #pragma unroll
@@ -630,6 +641,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
               f32x4{oacc[rh][mb][4 * g4] * inv, oacc[rh][mb][4 * g4 + 1] * inv, oacc[rh][mb][4 * g4 + 2] * inv,
                     oacc[rh][mb][4 * g4 + 3] * inv};
       if (hh == 0) a.part_lse[prow * a.s.hq + head] = lse;
+    }
+  }
+  if (direct) {
+    constexpr int CPRO = RB / 16, RPIO = 64 / CPRO;   // 16-byte chunks per row, rows per instruction
+    const int ch = lane % CPRO;
+#pragma unroll
+    for (int k = 0; k < 32 * NH / RPIO; ++k) {
+      const int rl = k * RPIO + lane / CPRO;          // staged row; its half is (k * RPIO) / 32
+      const int rh = (k * RPIO) / 32;
+      const int r = __shfl(row[rh], rl % 32);
+      const int ok = __shfl((int)row_ok[rh], rl % 32);
+      const u32x4 v = *(const u32x4*)(ot + rl * OS + 16 * ch);
+      if (ok) *(u32x4*)((uint8_t*)a.O + ((size_t)r * a.s.hq + head) * RB + 16 * ch) = v;
     }
   }
 }
