@@ -1209,19 +1209,55 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
       for (int mb = 0; mb < DB; ++mb) pin_a(dq[rh][mb]);
   }
 
+  // dQ rows leave as whole fp32 rows: each wave stages one 32-row half at a time in its own part of
+  // the LDS ring (free once every wave has finished the dQ products above; padded row stride QS),
+  // then copies it out 16 bytes per lane, two rows per instruction.  The destination of staged
+  // row r comes from lane r of the half.
+  // (Forms whose staged halves would not fit the ring store straight from the accumulators.)
+  constexpr int QS = D * 4 + 16;
+  constexpr int CPRQ = D * 4 / 16, RPIQ = 64 / CPRQ;   // 16-byte chunks per row, rows per instruction
   const float scale = a.s.scale;
+  if constexpr (NW * 32 * QS > NS * 2 * TB) {
+#pragma unroll
+    for (int rh = 0; rh < NH; ++rh) {
+      if (!row_ok[rh]) continue;
+      float* dst = it.part < 0 ? a.dQ + ((size_t)row[rh] * a.s.hq + head) * D
+                               : a.part_dq + (((size_t)it.part + ridx[rh]) * a.s.hq + head) * D;
+#pragma unroll
+      for (int mb = 0; mb < DB; ++mb)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4)
+          *(f32x4*)(dst + 32 * mb + 8 * g4 + 4 * hh) =
+              f32x4{dq[rh][mb][4 * g4] * scale, dq[rh][mb][4 * g4 + 1] * scale, dq[rh][mb][4 * g4 + 2] * scale,
+                    dq[rh][mb][4 * g4 + 3] * scale};
+    }
+    return;
+  }
+  uint8_t* qt = &smem[0][0][0] + wave * 32 * QS;
+  __syncthreads();
 #pragma unroll
   for (int rh = 0; rh < NH; ++rh) {
-    if (!row_ok[rh]) continue;
-    float* dst = it.part < 0 ? a.dQ + ((size_t)row[rh] * a.s.hq + head) * D
-                             : a.part_dq + (((size_t)it.part + ridx[rh]) * a.s.hq + head) * D;
+    uint8_t* qrow = qt + l32 * QS;
 #pragma unroll
     for (int mb = 0; mb < DB; ++mb)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4)
-        *(f32x4*)(dst + 32 * mb + 8 * g4 + 4 * hh) =
+        *(f32x4*)(qrow + 4 * (32 * mb + 8 * g4 + 4 * hh)) =
             f32x4{dq[rh][mb][4 * g4] * scale, dq[rh][mb][4 * g4 + 1] * scale, dq[rh][mb][4 * g4 + 2] * scale,
                   dq[rh][mb][4 * g4 + 3] * scale};
+    const size_t dsto = it.part < 0 ? ((size_t)row[rh] * a.s.hq + head) * D
+                                    : (((size_t)it.part + ridx[rh]) * a.s.hq + head) * D;
+    float* const base = it.part < 0 ? a.dQ : a.part_dq;
+    const int ch = lane % CPRQ;
+#pragma unroll
+    for (int k = 0; k < 32 / RPIQ; ++k) {
+      const int rl = k * RPIQ + lane / CPRQ;
+      const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)dsto, rl);
+      const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(dsto >> 32), rl);
+      const int ok = __shfl((int)row_ok[rh], rl);
+      const u32x4 v = *(const u32x4*)(qt + rl * QS + 16 * ch);
+      if (ok) *(u32x4*)(base + (((size_t)hi << 32) | lo) + 4 * ch) = v;
+    }
   }
 }
 
