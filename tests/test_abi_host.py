@@ -8,7 +8,9 @@
 * reference counts (Sec. 5.2) and the adaptive-block example (Sec. 5.1).
 """
 import ctypes
+import json
 import os
+import pathlib
 import re
 
 import numpy as np
@@ -116,26 +118,28 @@ def test_calls_before_upload_fail(base):
 
 # --------------------------------------------------------------------------- paper structure examples
 
+GOLDEN = json.loads((pathlib.Path(__file__).parent / "golden" / "paper_structure_examples.json").read_text())
+
+
 def test_refcounts_of_the_dbc_example():
-    # Sec. 5.2 / Fig. "Generation_Prefix_Tree": samples a, b, c, d; root read by all four,
-    # a second block read by a, b, c, a third block read by a only.
-    # Tree: root -> X -> {Ya, Yb, Yc}; root -> Yd.  Samples end at Ya, Yb, Yc, Yd.
-    wl = W.custom([-1, 0, 1, 1, 1, 0], [6, 4, 3, 2, 5, 4], [2, 3, 4, 5], tensors=False, seed=1)
+    # Sec. 5.2 / Fig. "Generation_Prefix_Tree" (tests/golden/paper_structure_examples.json)
+    ex = GOLDEN["dbc_example"]
+    wl = W.custom(ex["parent"], ex["seg_len_illustrative"], ex["samples"], tensors=False, seed=1)
     t = P.Tree.from_workload(wl)
-    assert list(t.refcounts()) == [4, 3, 1, 1, 1, 1]
+    assert list(t.refcounts()) == ex["refcounts"]
 
 
 def test_adaptive_block_example():
-    # Sec. 5.1 / Fig. "Block_Management": two 32-token sequences share tokens 0..27 and diverge at 28..31.
-    # Adaptive blocks: one 28-token shared block plus two 4-token blocks, no padding.
-    aba = W.custom([-1, 0, 0], [28, 4, 4], [1, 2], tensors=False, block_policy=W.blocks_exact)
+    # Sec. 5.1 / Fig. "Block_Management" (tests/golden/paper_structure_examples.json)
+    ex = GOLDEN["adaptive_block_example"]
+    aba = W.custom(ex["parent"], ex["seg_len"], ex["samples"], tensors=False, block_policy=W.blocks_exact)
     t = P.Tree.from_workload(aba)
-    assert list(aba.tree.blk_len) == [28, 4, 4] and aba.tree.pool_slots == 36
-    assert t.info["pad_slots"] == 0 and t.info["unshared_tokens"] == 64
-    # fixed 32-token blocks on the same tree: 3 blocks of 32 slots, 60 of them padding
-    fixed = W.custom([-1, 0, 0], [28, 4, 4], [1, 2], tensors=False, block_policy=lambda L: W.blocks_fixed(L, 32))
+    assert list(aba.tree.blk_len) == ex["adaptive"]["blk_len"] and aba.tree.pool_slots == ex["adaptive"]["pool_slots"]
+    assert t.info["pad_slots"] == ex["adaptive"]["pad_slots"] and t.info["unshared_tokens"] == ex["unshared_tokens"]
+    # fixed 32-token blocks on the same tree: no sharing inside a block, padding instead
+    fixed = W.custom(ex["parent"], ex["seg_len"], ex["samples"], tensors=False, block_policy=lambda L: W.blocks_fixed(L, 32))
     t2 = P.Tree.from_workload(fixed)
-    assert fixed.tree.pool_slots == 96 and t2.info["pad_slots"] == 60
+    assert fixed.tree.pool_slots == ex["fixed_32"]["pool_slots"] and t2.info["pad_slots"] == ex["fixed_32"]["pad_slots"]
 
 
 def test_named_config_plan_sizes():
