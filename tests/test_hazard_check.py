@@ -40,3 +40,10 @@ def test_operand_written_by_valu_needs_two_wait_states():
 def test_branches_are_followed():
     lines = [MF, "s_cbranch_scc1 .LBB0_2", "s_nop 15", ".LBB0_2:", "v_mov_b32_e32 v40, v5"]
     assert kinds(lines) == ["R1 mfma->other"]
+
+
+def test_valu_write_into_pending_result_across_a_block_is_flagged():
+    # an MFMA whose result has no reader, then the next block reuses one of its registers
+    lines = [MF, "s_branch .LBB0_3", ".LBB0_3:", "v_or_b32_e32 v4, s6, v0"]
+    assert kinds(lines) == ["R1 mfma->other"]
+    assert kinds([MF, "s_nop 11", "s_branch .LBB0_3", ".LBB0_3:", "v_or_b32_e32 v4, s6, v0"]) == []
