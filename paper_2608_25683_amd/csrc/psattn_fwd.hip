@@ -23,8 +23,10 @@
 #ifndef PSATTN_FWD_NH
 #define PSATTN_FWD_NH 1
 #endif
+// fragment prefetch distance of the main kernel, in MFMA pairs (6 measured best with two
+// wavefronts per SIMD, within 256 registers)
 #ifndef PSATTN_FWD_PF
-#define PSATTN_FWD_PF 4
+#define PSATTN_FWD_PF (PSATTN_FWD_NH == 1 ? 6 : 4)
 #endif
 
 namespace psattn {
