@@ -38,6 +38,15 @@ def test_random_forest_forced_splits(seed):
     H.check_full(wl, H.run_gpu(wl, opts={"fwd_kv_split": 64, "bwd_q_chunk": 32}), H.run_oracle(wl))
 
 
+# split key ranges (forward LSE merge) and split consumer lists (dK/dV and dQ reductions) with
+# one head per item and 256-row tiles (G = 5), MHA at d = 64, and G = 8
+@pytest.mark.parametrize("hq,hkv,d", [(5, 1, 128), (4, 4, 64), (8, 1, 64)])
+def test_forced_splits_head_layouts(hq, hkv, d):
+    wl = W.random_forest(350 + hq, max_nodes=6, max_seg=300, hq=hq, hkv=hkv, d=d, dtype="bf16")
+    _say(f"splits hq={hq} hkv={hkv} d={d} rows={wl.tree.num_rows}")
+    H.check_full(wl, H.run_gpu(wl, opts={"fwd_kv_split": 128, "bwd_q_chunk": 64}), H.run_oracle(wl))
+
+
 @pytest.mark.parametrize("hq,hkv,d", [(5, 1, 128), (8, 8, 64), (2, 1, 64), (12, 2, 128), (16, 2, 64), (3, 1, 128), (16, 1, 128)])
 def test_head_layouts(hq, hkv, d):
     wl = W.random_forest(400 + hq, max_nodes=5, max_seg=70, hq=hq, hkv=hkv, d=d, dtype="bf16")
