@@ -53,12 +53,26 @@ def compare(name, got, ref, dtype, mask=None):
     return maxabs, rel
 
 
+# softmax rows renormalised with the GPU's LSE sum to 1: sum_j exp(S_ij - LSE_gpu,i) equals
+# exp(LSE_i - LSE_gpu,i) with the fp64 LSE_i of the oracle.  fp32: the bound of the fp32 parity
+# (an LSE error of 1e-5 moves the sum by 1e-5; an fp32 LSE near 10 is itself only good to 5e-7)
+ROWSUM_TOL = {"bf16": 1e-2, "fp32": 1e-5}
+
+
+def check_rowsums(lse_gpu, lse_ref, dtype):
+    dev = np.abs(np.exp(lse_ref - lse_gpu) - 1.0)
+    worst = float(dev.max()) if dev.size else 0.0
+    assert worst <= ROWSUM_TOL[dtype], f"softmax rows with the GPU LSE sum to 1 +- {worst:.3g} (<= {ROWSUM_TOL[dtype]})"
+    return worst
+
+
 def check_full(wl, gpu, ref):
     Og, LSEg, dQg, dKg, dVg = gpu
     Or, LSEr, dQr, dKr, dVr = ref
     res = {}
     for name, g, r in (("O", Og, Or), ("LSE", LSEg, LSEr), ("dQ", dQg, dQr), ("dK", dKg, dKr), ("dV", dVg, dVr)):
         res[name] = compare(name, g, r, wl.dtype)
+    res["rowsum"] = check_rowsums(LSEg, LSEr, wl.dtype)
     # pool slots holding no token get exactly zero
     pad = np.setdiff1d(np.arange(wl.tree.pool_slots), wl.tree.row_slots())
     assert np.all(dKg[pad] == 0) and np.all(dVg[pad] == 0)
@@ -105,7 +119,7 @@ def check_sampled(wl, gpu, kv_heads=(0,), seed=0):
     o_r, lse_r = O.rows_forward(ti, wl.Q, wl.K, wl.V, wl.scale, rows, heads)
     dq_r = O.rows_dq(ti, wl.Q, wl.K, wl.V, wl.dO, wl.scale, rows, heads)
     res = {"O": compare("O", Og[rows], o_r, wl.dtype), "LSE": compare("LSE", LSEg[:, rows], lse_r, wl.dtype),
-           "dQ": compare("dQ", dQg[rows], dq_r, wl.dtype)}
+           "rowsum": check_rowsums(LSEg[:, rows], lse_r, wl.dtype), "dQ": compare("dQ", dQg[rows], dq_r, wl.dtype)}
     keys = sample_keys(wl, seed=seed)
     slots = t.row_slots()[keys]
     dk_g, dv_g, dk_r, dv_r = [], [], [], []
