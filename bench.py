@@ -122,8 +122,8 @@ def copy_calibration(mib):
 def main():
     a = parse()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the prefix-shared attention path is a single-GPU kernel "
-              "(multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
+        print("bench.py measures one GPU only: the prefix-shared attention path runs on a single GPU, "
+              "and sharding a forest across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
     if a.copy_calibration_mib:
         copy_calibration(a.copy_calibration_mib)
