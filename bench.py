@@ -34,7 +34,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c2", help="workload: c1..c5 (c2 is the metric's workload)")
+    ap.add_argument("--config", default="c2",
+                    help="workload: c1..c5 (c2 is the metric's workload), or c2-small (the small-suffix probe)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample (0 disables the cpu_baseline leg)")
     ap.add_argument("--no-profile", action="store_true", help="do not bracket kernels with timing events")

@@ -41,6 +41,8 @@ CONFIGS = {
            "step-wise RL chains, 32q/8kv d128 bf16: 8 trajectories x 8 steps of U[256,1024]; adaptive blocks {256,64,16}"),
     "c4": (4, 32, 8, 128, "bf16", 0.5,
            "tree sampling, 32q/8kv d128 bf16: root 2048, branching 4, depth 3 (64 leaves), segments U[128,768]; per-node block size"),
+    "c2-small": (6, 32, 8, 128, "bf16", 0.5,
+                 "small-suffix probe, Llama-3-8B-shaped GQA 32q/8kv d128 bf16: prefix 4096 + 256 branches of 16; page block 16"),
     "c5": (5, 40, 8, 128, "bf16", 0.5,
            "Qwen2.5-32B-shaped 40q/8kv d128 bf16: 32 trees depth 2-4, branching 2-6, log-normal segments; tree-step samples; exact-length blocks"),
 }
@@ -243,6 +245,13 @@ def _struct_c2(rng):
     return parent, seg, [blocks_fixed(L, 64) for L in seg], list(range(1, 17))
 
 
+def _struct_c2_small(rng):
+    # few queries per branch against a long shared prefix: the gather-bound end of the path
+    parent = [-1] + [0] * 256
+    seg = [4096] + [16] * 256
+    return parent, seg, [blocks_fixed(L, 16) for L in seg], list(range(1, 257))
+
+
 def _struct_c3(rng):
     parent, seg = [], []
     for traj in range(8):
@@ -335,7 +344,7 @@ def _struct_c5(rng, budget: int = C5_NU_BUDGET):
     return parent, seg, [blocks_exact(L) for L in seg], samples, K
 
 
-_STRUCT = {"c1": _struct_c1, "c2": _struct_c2, "c3": _struct_c3, "c4": _struct_c4}
+_STRUCT = {"c1": _struct_c1, "c2": _struct_c2, "c2-small": _struct_c2_small, "c3": _struct_c3, "c4": _struct_c4}
 
 
 def tree_stats(tree: Tree, hq: int, d: int) -> dict:

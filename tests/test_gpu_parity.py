@@ -141,7 +141,7 @@ def test_pool_order_and_padding_do_not_change_results():
 
 # --------------------------------------------------------------------------- full-size workloads (sampled)
 
-@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["c2", "c2-small", "c3", "c4", "c5"])
 def test_full_size_sampled(name):
     _say(f"{name}: generating")
     wl = W.make(name)

@@ -8,6 +8,8 @@ from paper_2608_25683_amd import workloads as W
 PINS = {
     "c1": (5, 4, 24, 384, 384, 768, 192, 49_344, None),
     "c2": (17, 16, 320, 20_480, 20_480, 81_920, 5_120, 83_896_320, None),
+    # 256 branches of 16 on a 4096-token root, blocks of 16: sum_nvis = 4096*4097/2 + 256*(16*4096 + 136)
+    "c2-small": (257, 256, 512, 8_192, 8_192, 1_052_672, 4_112, 25_202_688, None),
     "c3": (64, 64, 389, 41_552, 40_998, 187_643, 5_901, 105_901_670, None),
     "c4": (85, 64, 1_099, 46_112, 42_109, 219_694, 4_100, 126_438_093, None),
     "c5": (127, 127, 127, 107_703, 107_703, 234_026, 7_192, 202_132_990, 2),
