@@ -284,7 +284,79 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     split_keys = std::max<int64_t>(16 * KV_TILE, per_cu / std::max(1, s.bmq) / KV_TILE * KV_TILE);
   }
   int64_t part_rows = 0;
+  // Sibling packing: children of one parent whose segments fill at most half a query tile share
+  // the key range [0, off) of their common prefix.  Their rows are packed (first fit, child
+  // order) into one tile for that range, and each node keeps an item of its own keys
+  // [off, off + seg).  A pack's partial rows: prefix piece j of the node at pack offset o at
+  // P + j*bmq + o, the node's own piece at P + npref*bmq + o, so that one merge record per node
+  // (part0 = P + o, npref + 1 parts) combines them.
+  std::vector<char> packed(N, 0);
+  std::vector<std::vector<int>> packs;
+  for (int p = 0; p < N; ++p) {
+    std::vector<int> cur;
+    int rows = 0;
+    auto flush = [&]() {
+      if (cur.size() >= 2) {
+        for (int c : cur) packed[c] = 1;
+        packs.push_back(cur);
+      }
+      cur.clear();
+      rows = 0;
+    };
+    for (int c : t->children[p]) {
+      if (2 * t->seg_len[c] > s.bmq) continue;
+      if (rows + t->seg_len[c] > s.bmq) flush();
+      cur.push_back(c);
+      rows += t->seg_len[c];
+    }
+    flush();
+  }
+  auto split_range = [&](int64_t nkv_total) {
+    return split_keys == INT64_MAX ? 1 : (int)((nkv_total + split_keys - 1) / split_keys);
+  };
+  for (const std::vector<int>& pk : packs) {
+    const int n0 = pk[0];
+    const int64_t pre = t->off[n0];   // the common prefix: every sibling starts at the same position
+    const int npref = split_range(pre);
+    const int32_t P = (int32_t)part_rows;
+    part_rows += (int64_t)(npref + 1) * s.bmq;
+    const int32_t q_pack = (int32_t)t->q_list.size();
+    int rows = 0;
+    for (int n : pk)
+      for (int a = 0; a < t->seg_len[n]; ++a) t->q_list.push_back((int32_t)(t->row_off[n] + a));
+    for (int j = 0; j < npref; ++j) {
+      const int64_t k0 = npref > 1 ? j * split_keys : 0;
+      const int64_t k1 = npref > 1 ? std::min(pre, (j + 1) * split_keys) : pre;
+      FTask f;
+      f.q_off = q_pack;
+      f.nq = (int32_t)(t->q_list.size() - q_pack);
+      f.kv_off = (int32_t)(kvoff[n0] + k0);
+      f.kv_pos0 = (int32_t)k0;
+      f.nkv = (int32_t)(k1 - k0);
+      f.min_qpos = (int32_t)pre;
+      f.part = P + j * s.bmq;
+      f.cost = (double)f.nq * (double)f.nkv + 4096.0;
+      ftasks.push_back(f);
+    }
+    for (int n : pk) {
+      const int32_t q_off = (int32_t)t->q_list.size();
+      for (int a = 0; a < t->seg_len[n]; ++a) t->q_list.push_back((int32_t)(t->row_off[n] + a));
+      merges.push_back({q_off, t->seg_len[n], P + rows, npref + 1});
+      FTask f;
+      f.q_off = q_off;
+      f.nq = t->seg_len[n];
+      f.kv_off = (int32_t)(kvoff[n] + pre);
+      f.kv_pos0 = (int32_t)pre;
+      f.nkv = t->seg_len[n];
+      f.min_qpos = (int32_t)pre;
+      f.part = P + npref * s.bmq + rows;
+      f.cost = (double)f.nq * (double)f.nkv + 4096.0;
+      ftasks.push_back(f);
+      rows += t->seg_len[n];
+    }
+  }
   for (int n = 0; n < N; ++n) {
+    if (packed[n]) continue;
     for (int a0 = 0; a0 < t->seg_len[n]; a0 += s.bmq) {
       int a1 = std::min<int>(t->seg_len[n], a0 + s.bmq);
       int nq = a1 - a0;

@@ -207,13 +207,26 @@ def _check_plan(wl, t):
                         cover[(h, r, k)] = cover.get((h, r, k), 0) + 1
     assert all(v == 1 for v in cover.values())
     assert len(cover) == len(visible) * wl.hq
-    # split pieces belong to a merge entry with the same rows
-    parts = {int(p) for p in fwd[:, 6] if p >= 0}
-    want = set()
+    # partial rows: each is written by one (item, head chunk) row, and the merge records read
+    # exactly the written rows, each for the query row that wrote it
+    written = {}
+    for q_off, nq, kv_off, nkv, kv_pos0, head0, part, nfull in fwd:
+        if part < 0:
+            continue
+        for i in range(nq):
+            key = (int(part + i), int(head0))
+            assert key not in written, "partial row written twice"
+            written[key] = int(q_list[q_off + i])
+    read = {}
     for q_off, nq, part0, nparts in merges:
         for j in range(nparts):
-            want.add(int(part0 + j * bmq))
-    assert parts == want
+            for i in range(nq):
+                read[int(part0 + j * bmq + i)] = int(q_list[q_off + i])
+    assert {p for p, _ in written} == set(read)
+    assert all(read[p] == r for (p, _), r in written.items())
+    # every row with partial results is merged exactly once
+    merged_rows = [int(q_list[q_off + i]) for q_off, nq, _, _ in merges for i in range(nq)]
+    assert len(merged_rows) == len(set(merged_rows))
 
     # dK/dV items: every visible pair once per query head (G heads per kv head)
     cover = {}
@@ -248,6 +261,22 @@ def test_plan_covers_tree_mask_exactly_once(seed):
     if seed % 2 == 0:
         opts = {"fwd_kv_split": 64 * (1 + seed % 3), "bwd_q_chunk": 32 * (1 + seed % 4)}
     t = P.Tree.from_workload(wl, opts=opts)
+    _check_plan(wl, t)
+
+
+SIBLINGS = dict(parent=[-1] + [0] * 12 + [1, 1, 1], seg_len=[300, 16, 9, 30, 1, 16, 16, 5, 20, 16, 16, 2, 31, 7, 12, 3],
+                samples=list(range(1, 16)))
+
+
+@pytest.mark.parametrize("opts", [{}, {"fwd_kv_split": 64, "bwd_q_chunk": 32}])
+def test_plan_packs_short_siblings(opts):
+    # short children of one parent share their prefix key range in one packed query tile
+    wl = W.custom(SIBLINGS["parent"], SIBLINGS["seg_len"], SIBLINGS["samples"], hq=8, hkv=2, tensors=False,
+                  block_policy=lambda L: W.blocks_fixed(L, 16))
+    t = P.Tree.from_workload(wl, opts=opts)
+    q, f = t.plan_array("q_list"), t.plan_array("fwd_items")
+    owner = np.repeat(np.arange(wl.tree.num_nodes), wl.tree.seg_len)
+    assert sum(len(set(owner[q[a:a + b]])) > 1 for a, b in f[:, :2]) > 0
     _check_plan(wl, t)
 
 

@@ -72,6 +72,9 @@ def test_c1_full_fp32():
 SMALL = {
     "c2s": dict(parent=[-1] + [0] * 5, seg=[300] + [150] * 5, samples=list(range(1, 6)), hq=8, hkv=2,
                 policy=lambda L: W.blocks_fixed(L, 64)),
+    # short siblings packed against their common prefix (the small-suffix case)
+    "c2ss": dict(parent=[-1] + [0] * 12 + [1, 1, 1], seg=[300, 16, 9, 30, 1, 16, 16, 5, 20, 16, 16, 2, 31, 7, 12, 3],
+                 samples=list(range(1, 16)), hq=8, hkv=2, policy=lambda L: W.blocks_fixed(L, 16)),
     "c3s": dict(parent=[-1, 0, 1, -1, 3, 4], seg=[70, 130, 95, 110, 33, 200], samples=list(range(6)), hq=8, hkv=2,
                 policy=W.blocks_greedy),
     "c4s": dict(parent=[-1, 0, 0, 1, 1, 2, 2], seg=[256, 40, 131, 77, 64, 9, 100], samples=[3, 4, 5, 6], hq=8,
@@ -88,6 +91,14 @@ def test_scaled_down_workloads(name):
                   block_policy=c["policy"])
     _say(f"scaled-down {name} rows={wl.tree.num_rows}")
     H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+
+
+def test_packed_siblings_with_split_prefix():
+    # the packed prefix piece itself split into several key ranges
+    c = SMALL["c2ss"]
+    wl = W.custom(c["parent"], c["seg"], c["samples"], hq=c["hq"], hkv=c["hkv"], d=128, dtype="bf16", seed=8,
+                  block_policy=c["policy"])
+    H.check_full(wl, H.run_gpu(wl, opts={"fwd_kv_split": 64, "bwd_q_chunk": 32}), H.run_oracle(wl))
 
 
 # degenerate trees: one-token nodes, many tiny siblings, a deep chain of one-token nodes, a
