@@ -1488,7 +1488,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kv_kernel(BwdArgs a) {
   const ReduceEntry e = a.plan.reduce[blockIdx.x];
   const int D = a.s.d;
   const size_t kv_stride = (size_t)a.s.hkv * D;
-  for (int idx = threadIdx.x; idx < e.nk * (D / 4); idx += blockDim.x) {
+  for (int idx = blockIdx.y * blockDim.x + threadIdx.x; idx < e.nk * (D / 4); idx += gridDim.y * blockDim.x) {
     const int k = idx / (D / 4), d4 = (idx % (D / 4)) * 4;
     f32x4 sk = f32x4{}, sv = f32x4{};
     for (int j = 0; j < e.nparts; ++j) {
@@ -1507,7 +1507,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_dq_kernel(BwdArgs a) {
   const MergeEntry e = a.plan.merge[blockIdx.x];
   const int D = a.s.d, hq = a.s.hq, bmq = a.s.bmq;
   const int per_row = hq * D / 4;
-  for (int idx = threadIdx.x; idx < e.nq * per_row; idx += blockDim.x) {
+  for (int idx = blockIdx.y * blockDim.x + threadIdx.x; idx < e.nq * per_row; idx += gridDim.y * blockDim.x) {
     const int i = idx / per_row, r = (idx % per_row) * 4;
     f32x4 acc = f32x4{};
     for (int j = 0; j < e.nparts; ++j)
@@ -1598,12 +1598,12 @@ hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st) {
 }
 
 hipError_t launch_bwd_reduce_kv(const BwdArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(bwd_reduce_kv_kernel, dim3(a.n_reduce), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(bwd_reduce_kv_kernel, dim3(a.n_reduce, kMergeSlices), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_bwd_reduce_dq(const BwdArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(bwd_reduce_dq_kernel, dim3(a.n_merge), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(bwd_reduce_dq_kernel, dim3(a.n_merge, kMergeSlices), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -42,6 +42,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 constexpr int IDX_BLK = 256;   // slot / row indices staged in LDS per block
+constexpr int kMergeSlices = 8; // workgroups per merge / reduction record (grid y)
 static_assert((IDX_BLK & (IDX_BLK - 1)) == 0, "staged index blocks are addressed modulo 2*IDX_BLK");
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {

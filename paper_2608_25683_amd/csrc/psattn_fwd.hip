@@ -745,33 +745,34 @@ __global__ __launch_bounds__(512) void fwd_f32_kernel(FwdArgs a) {
 // log-sum-exp merge of split forward pieces, fixed piece order
 template <bool BF16>
 __global__ __launch_bounds__(256) void fwd_merge_kernel(FwdArgs a) {
+  // D/4 lanes per (row, head), 4 elements each (coalesced rows); blockIdx.y slices the pairs
   const MergeEntry e = a.plan.merge[blockIdx.x];
   const int hq = a.s.hq, D = a.s.d, bmq = a.s.bmq;
-  for (int idx = threadIdx.x; idx < e.nq * hq; idx += blockDim.x) {
-    const int i = idx / hq, h = idx % hq;
+  const int lanes = D / 4, per_pass = 256 / lanes;
+  const int d4 = 4 * (threadIdx.x % lanes);
+  for (int pr = blockIdx.y * per_pass + threadIdx.x / lanes; pr < e.nq * hq; pr += gridDim.y * per_pass) {
+    const int i = pr / hq, h = pr % hq;
     const int row = a.plan.q_list[e.q_off + i];
     float m = kNegInf;
     for (int j = 0; j < e.nparts; ++j) m = fmaxf(m, a.part_lse[((size_t)e.part0 + (size_t)j * bmq + i) * hq + h]);
     float wsum = 0.f;
     for (int j = 0; j < e.nparts; ++j) wsum += expf(a.part_lse[((size_t)e.part0 + (size_t)j * bmq + i) * hq + h] - m);
     const float lse = m + logf(wsum);
-    a.LSE[(size_t)h * a.s.ns + row] = lse;
-    for (int d4 = 0; d4 < D; d4 += 4) {
-      f32x4 acc = f32x4{};
-      for (int j = 0; j < e.nparts; ++j) {
-        const size_t prow = (size_t)e.part0 + (size_t)j * bmq + i;
-        const float w = expf(a.part_lse[prow * hq + h] - lse);
-        const f32x4 x = *(const f32x4*)(a.part_o + (prow * hq + h) * D + d4);
-        acc += w * x;
-      }
-      if (BF16) {
-        u32x2 w2;
-        w2[0] = pack2(acc[0], acc[1]);
-        w2[1] = pack2(acc[2], acc[3]);
-        *(u32x2*)((bf16_t*)a.O + ((size_t)row * hq + h) * D + d4) = w2;
-      } else {
-        *(f32x4*)((float*)a.O + ((size_t)row * hq + h) * D + d4) = acc;
-      }
+    if (d4 == 0) a.LSE[(size_t)h * a.s.ns + row] = lse;
+    f32x4 acc = f32x4{};
+    for (int j = 0; j < e.nparts; ++j) {
+      const size_t prow = (size_t)e.part0 + (size_t)j * bmq + i;
+      const float w = expf(a.part_lse[prow * hq + h] - lse);
+      const f32x4 x = *(const f32x4*)(a.part_o + (prow * hq + h) * D + d4);
+      acc += w * x;
+    }
+    if (BF16) {
+      u32x2 w2;
+      w2[0] = pack2(acc[0], acc[1]);
+      w2[1] = pack2(acc[2], acc[3]);
+      *(u32x2*)((bf16_t*)a.O + ((size_t)row * hq + h) * D + d4) = w2;
+    } else {
+      *(f32x4*)((float*)a.O + ((size_t)row * hq + h) * D + d4) = acc;
     }
   }
 }
@@ -814,8 +815,9 @@ hipError_t launch_fwd_main(const FwdArgs& a, bool bf16, hipStream_t st) {
 }
 
 hipError_t launch_fwd_merge(const FwdArgs& a, bool bf16, hipStream_t st) {
-  if (bf16) hipLaunchKernelGGL((fwd_merge_kernel<true>), dim3(a.n_merge), dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((fwd_merge_kernel<false>), dim3(a.n_merge), dim3(256), 0, st, a);
+  const dim3 grid(a.n_merge, kMergeSlices);
+  if (bf16) hipLaunchKernelGGL((fwd_merge_kernel<true>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((fwd_merge_kernel<false>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
