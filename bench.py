@@ -25,8 +25,12 @@ METRIC = "effective fwd+bwd attention tokens/sec (unshared-equiv) + % bf16 MFMA 
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_25683_amd", "csrc", f) for f in
                ("psattn_device.h", "psattn_fwd.hip", "psattn_bwd.hip")]
 
-# matmul flops each kernel executes per visible (query, key) pair and query head, per unit of head_dim
-FLOPS_PER_PAIR_PER_D = {"fwd_main": 4, "bwd_kv": 8, "bwd_dq": 6}
+# algorithmic matmul flops of each kernel per visible (query, key) pair and query head, per unit
+# of head_dim, in the FlashAttention convention that F_alg = 14 d per pair follows: forward S and
+# P V (4 d); backward S recompute, dP, dV, dK (8 d, the dK/dV kernel) and dQ (2 d).  The dQ kernel
+# executes 6 d: it recomputes S and dP (the deterministic, atomic-free split of the backward).
+FLOPS_PER_PAIR_PER_D = {"fwd_main": 4, "bwd_kv": 8, "bwd_dq": 2}
+EXEC_FLOPS_PER_PAIR_PER_D = {"fwd_main": 4, "bwd_kv": 8, "bwd_dq": 6}
 
 
 def parse():
@@ -80,10 +84,24 @@ def cpu_baseline(wl, seconds):
         threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        blas = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{blas.get('name', '?')} {blas.get('version', '')}".strip()
+    except Exception:
+        blas = "unknown"
     t = wl.tree
     G = wl.hq // wl.hkv
     done = []   # (sample, heads)
     tokens = 0.0
+    flops = 0.0   # algorithmic: 14 d per visible (query, key) pair and head, as F_alg
     t0 = time.perf_counter()
     for s, idx in enumerate(O.sample_rows(t.parent, t.seg_len, t.row_off, t.sample_end)):
         heads = 0
@@ -96,6 +114,7 @@ def cpu_baseline(wl, seconds):
             O.causal_bwd(q, k, v, o, lse, do, wl.scale)
             heads += 1
             tokens += len(idx) / wl.hq
+            flops += 14.0 * wl.d * len(idx) * (len(idx) + 1) / 2
             if time.perf_counter() - t0 >= seconds:
                 break
         done.append((s, len(idx), heads))
@@ -104,7 +123,10 @@ def cpu_baseline(wl, seconds):
     el = time.perf_counter() - t0
     desc = "; ".join(f"sample {s} ({n} tokens) x {h} heads" for s, n, h in done)
     return {"value": tokens / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{desc} of {wl.hq} query heads each, fwd+bwd, fp64 numpy; {el:.1f} s wall"}
+            "sample": f"{desc} of {wl.hq} query heads each, fwd+bwd, fp64 numpy; {el:.1f} s wall",
+            "cpu_model": cpu_model, "blas": blas, "gflops_alg": flops / el / 1e9,
+            "note": "the expanded (unshared) fp64 oracle: every sample recomputed in full; tokens count "
+                    "one sample token over all query heads as one token"}
 
 
 def copy_calibration(mib):
@@ -167,19 +189,20 @@ def main():
     torch.cuda.synchronize()
     P.psattn_profile_reset()
     P.psattn_profile_enable(not a.no_profile)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    ev0.record()
-    for _ in range(a.steps):
+    evs[0].record()
+    for k in range(a.steps):
         step()
-    ev1.record()
+        evs[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     P.psattn_profile_enable(False)
-    ms_total = ev0.elapsed_time(ev1)
+    ms_total = evs[0].elapsed_time(evs[-1])
     ms_step = ms_total / a.steps
+    per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(a.steps))
+    ms_median = per_step[len(per_step) // 2] if a.steps % 2 else 0.5 * (per_step[a.steps // 2 - 1] + per_step[a.steps // 2])
     kern = P.psattn_profile_read() if not a.no_profile else {}
     P.psattn_profile_reset()
 
@@ -198,7 +221,8 @@ def main():
             achieved = flops / (avg_ms / 1e3) / 1e12
             roof = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                     "frac": achieved / peak, "traffic": kernel_traffic(dom, a.config),
-                    "flops_per_launch": flops, "avg_ms": avg_ms}
+                    "flops_per_launch": flops, "avg_ms": avg_ms,
+                    "executed_flops_per_launch": EXEC_FLOPS_PER_PAIR_PER_D[dom] * d * hq * st["sum_nvis"]}
     out = {
         "metric": METRIC,
         "value": value,
@@ -219,6 +243,10 @@ def main():
                       "flops": "14*d*Hq*sum_visible_pairs"},
         "roofline": roof,
         "kernels": per_kernel,
+        "timing": {"ms_per_step": "mean of the timed steps (hipEvent on the stream, total / steps)",
+                   "ms_per_step_median": ms_median, "ms_per_step_min": per_step[0], "ms_per_step_max": per_step[-1],
+                   "caches": "L2 and MALL are not flushed between steps; inputs resident in HBM",
+                   "excluded": "plan build and upload (once per tree, reused by every layer)"},
         "plan_ms": t_plan * 1e3,
         "wall_s_timed": wall,
     }

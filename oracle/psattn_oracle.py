@@ -299,12 +299,14 @@ def rows_dq(ti: TreeIndex, Q, K, V, dO, scale, rows: Sequence[int], heads: Seque
     return out
 
 
-def keys_dkdv(ti: TreeIndex, Q, K, V, dO, scale, key_rows: Sequence[int], kv_head: int):
+def keys_dkdv(ti: TreeIndex, Q, K, V, dO, scale, key_rows: Sequence[int], kv_head: int, forward_out=None):
     """dK, dV [len(key_rows), d] of selected key rows for one kv head (fp64).
 
     Consumers of key row j (node m, position b) are rows of m at positions
     >= b and every row of every descendant of m; each consumer contributes
-    through all G query heads that read kv head ``kv_head``.
+    through all G query heads that read kv head ``kv_head``.  If
+    ``forward_out`` is a dict, the consumers' forward results are left in it:
+    forward_out[m] = (consumer rows, O [rows, G, d], LSE [G, rows]).
     """
     Hq, Hkv = Q.shape[1], K.shape[1]
     G = Hq // Hkv
@@ -325,19 +327,21 @@ def keys_dkdv(ti: TreeIndex, Q, K, V, dO, scale, key_rows: Sequence[int], kv_hea
                 cons.append(np.arange(ti.row_off[c], ti.row_off[c] + ti.seg_len[c]))
         cons = np.concatenate(cons)
         O, LSE = rows_forward(ti, Q, K, V, scale, cons, heads)
+        if forward_out is not None:
+            forward_out[m] = (cons, O, LSE)
         qpos = ti.off[ti.row_node[cons]] + (cons - ti.row_off[ti.row_node[cons]])
-        for i in kidx:
-            j = key_rows[i]
-            kpos = ti.off[m] + (j - ti.row_off[m])
-            vis = qpos >= kpos
-            kj = _as64(K[j, kv_head])
-            vj = _as64(V[j, kv_head])
-            for hi, h in enumerate(heads):
-                q = _as64(Q[cons[vis], h])
-                do = _as64(dO[cons[vis], h])
-                p = np.exp(scale * (q @ kj) - LSE[hi, vis])
-                dp = do @ vj
-                delta = np.sum(do * O[vis, hi], axis=1)
-                dV[i] += p @ do
-                dK[i] += scale * ((p * (dp - delta)) @ q)
+        kidx = np.asarray(kidx)
+        kpos = ti.off[m] + (key_rows[kidx] - ti.row_off[m])
+        vis = qpos[:, None] >= kpos[None, :]                        # [consumers, keys]
+        kj = _as64(K[key_rows[kidx], kv_head])                       # [keys, d]
+        vj = _as64(V[key_rows[kidx], kv_head])
+        for hi, h in enumerate(heads):
+            q = _as64(Q[cons, h])
+            do = _as64(dO[cons, h])
+            s = np.where(vis, scale * (q @ kj.T), -np.inf)
+            p = np.exp(s - LSE[hi][:, None])                         # P_ij of every consumer i, key j
+            dp = do @ vj.T                                           # dP_ij = dO_i . v_j
+            delta = np.sum(do * O[:, hi], axis=1)                    # Delta_i = dO_i . O_i
+            dV[kidx] += p.T @ do
+            dK[kidx] += scale * ((p * (dp - delta[:, None])).T @ q)
     return dK, dV

@@ -9,9 +9,8 @@
 // operands (dO^T, Q^T) come from transposing LDS reads of the row-major tiles.  The main form
 // (bwd_kv_bf16_1w_kernel) runs one wavefront per SIMD, wave w keeping keys 32w..32w+31 of K and
 // V and their dK/dV accumulators in registers, and streams Q/dO rows and the LSE/Delta values
-// global -> LDS directly into a five-step ring; the older eight-wavefront form (bwd_kv_bf16_kernel)
-// remains for pools and tensors beyond 32-bit byte offsets.  Consumer-row indices are staged in
-// LDS 256 at a time.
+// global -> LDS directly into a five-step ring.  Consumer-row indices are staged in LDS 256 at a
+// time.
 //
 // bf16 dQ kernel: the same items as the forward kernel and its structure (NH 32-row halves per
 // wave); recomputes S^T and dP^T per key tile and accumulates dQ^T += K^T dS^T, K^T again from
@@ -31,393 +30,16 @@
 #define PSATTN_DQ_PF (PSATTN_DQ_NH == 1 ? 3 : 4)
 #endif
 
+// Remainder products in the dK/dV kernel on steps with large P or dS (1); 0 rounds P and dS once
+// everywhere (a timing variant: its error grows with the number of consumers of a key)
+#ifndef PSATTN_KV_REM
+#define PSATTN_KV_REM 1
+#endif
+
 namespace psattn {
 namespace {
 
 using namespace dev;
-
-// 8 wavefronts: wave w owns keys 32*(w%4) .. +31 of the tile and, within each pipeline stage of
-// 32 rows x 2 query heads, the head w/4; the two waves of a key group add their dK/dV partial
-// sums in a fixed order at the end.
-template <int D>
-__global__ __launch_bounds__(512) void bwd_kv_bf16_kernel(BwdArgs a) {
-  constexpr int RB = D * 2;
-  constexpr int CPR = D / 8;
-  constexpr int RPI = 64 / CPR;
-  constexpr int QB = Q_SUB * RB;              // bytes per Q or dO subtile of one head
-  constexpr int NI = Q_SUB / RPI;             // copy instructions per subtile and tensor
-  constexpr int KS = D / 16, DB = D / 32;
-  constexpr int SPB = IDX_BLK / Q_SUB;        // subtiles per staged row block
-  constexpr int HPS = 2;                      // query heads per pipeline stage
-  constexpr int KVB = BKV_TILE * RB;          // bytes of the K (or V) tile
-  constexpr int STB = 2 * HPS * 2 * QB;       // bytes of both stages
-  static_assert(2 * KVB + STB >= 4 * 32 * D * 4 * 2, "pair reduction buffer");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * KVB + STB];   // K | V | stages[2][HPS][Q|dO]
-  __shared__ __attribute__((aligned(16))) float s_stat[2][HPS][2][Q_SUB];  // [stage][head][LSE*log2e | Delta]
-  __shared__ int s_row[2][IDX_BLK];
-  __shared__ int s_qpos[2][IDX_BLK];
-  __shared__ int s_slot[BKV_TILE];
-  uint8_t* const s_k = smem;
-  uint8_t* const s_v = smem + KVB;
-  uint8_t* const s_st = smem + 2 * KVB;
-  auto stage_q = [&](int st, int j) { return s_st + ((st * HPS + j) * 2 + 0) * QB; };
-  auto stage_do = [&](int st, int j) { return s_st + ((st * HPS + j) * 2 + 1) * QB; };
-
-  const BkvItem it = a.plan.bkv[blockIdx.x];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, hh = lane >> 5;
-  const int kg = wave & 3, hp = wave >> 2;    // key group, head within a stage
-  const int hk = it.hk, G = a.s.g, hq = a.s.hq, ns = a.s.ns;
-  const int nq = it.nq;
-  const int* ql = a.plan.q_list + it.q_off;
-  const size_t kv_stride = (size_t)a.s.hkv * D;
-  const int ngrp = (G + HPS - 1) / HPS;       // stages per 32-row subtile
-  const int crow = lane / CPR, cpc = lane % CPR;
-
-  if (tid < BKV_TILE) s_slot[tid] = a.plan.kv_list[it.kv_off + min(tid, it.nk - 1)];
-  if (tid < IDX_BLK) {
-    const int r = ql[min(tid, nq - 1)];
-    s_row[0][tid] = r;
-    s_qpos[0][tid] = tid < nq ? a.plan.row_pos[r] : -1;
-  }
-  int pre_row = 0, pre_qpos = -1;
-  if (tid < IDX_BLK && nq > IDX_BLK) {
-    pre_row = ql[min(IDX_BLK + tid, nq - 1)];
-    pre_qpos = IDX_BLK + tid < nq ? a.plan.row_pos[pre_row] : -1;
-  }
-  __syncthreads();
-  // K and V rows of the tile into LDS (row-major, swizzled): B operands of S = Q K^T, dP = dO V^T
-#pragma unroll
-  for (int i = 0; i < BKV_TILE / RPI / 8; ++i) {
-    const int k = wave + 8 * i;
-    const int r = k * RPI + crow;
-    const size_t go = (size_t)s_slot[r] * kv_stride + (size_t)hk * D + ((cpc ^ swz<D>(r)) << 3);
-    copy16_to_lds((const bf16_t*)a.K + go, s_k + k * 1024);
-    copy16_to_lds((const bf16_t*)a.V + go, s_v + k * 1024);
-  }
-
-  const int kidx = 32 * kg + l32;
-  const int kpos = it.kv_pos0 + kidx;
-  f32x16 dk[DB], dv[DB];
-#pragma unroll
-  for (int nb = 0; nb < DB; ++nb) {
-    dk[nb] = f32x16{};
-    dv[nb] = f32x16{};
-  }
-
-  const int nsub = (nq + Q_SUB - 1) / Q_SUB;
-  const int nsteps = nsub * ngrp;
-  auto issue = [&](int step) {
-    const int st = step & 1, sub = step / ngrp, h0 = (step % ngrp) * HPS;
-    const int nh = min(HPS, G - h0);
-    const int* rows = &s_row[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
-    // 2 heads x 2 tensors x NI copy instructions over 8 waves
-#pragma unroll
-    for (int i = 0; i < (HPS * 2 * NI + 7) / 8; ++i) {
-      const int k = wave + 8 * i;              // (head, tensor, instruction)
-      const int jh = k / (2 * NI), tens = (k / NI) & 1, ins = k % NI;
-      if (k < HPS * 2 * NI && jh < nh) {
-        const int r = ins * RPI + crow;
-        const size_t go = ((size_t)rows[r] * hq + hk * G + h0 + jh) * D + ((cpc ^ swz<D>(r)) << 3);
-        copy16_to_lds((const bf16_t*)(tens ? a.dO : a.Q) + go, (tens ? stage_do(st, jh) : stage_q(st, jh)) + ins * 1024);
-      }
-    }
-    if (wave < nh) {   // wave j brings LSE*log2e (lanes 0-31) and Delta (lanes 32-63) of head h0 + j
-      const float* src = hh ? a.delta : a.lse2;
-      copy4_to_lds(src + (size_t)(hk * G + h0 + wave) * ns + rows[l32], &s_stat[st][wave][0][0]);
-    }
-  };
-
-  const float c = a.s.scale * kLog2e;
-  const int arow = l32 * RB, asw = swz<D>(l32);
-  const int krow = (32 * kg + l32) * RB;      // this lane's key row in the K / V tiles (same swizzle)
-  const int r4 = (lane & 15) >> 2, jq = lane & 3, dsub = 16 * ((lane >> 4) & 1);
-  const int tcol = (dsub + 4 * jq) >> 3, tbyte = 8 * (jq & 1);
-  const int trow0 = (4 * hh + r4) * RB, tsw0 = swz<D>(4 * hh + r4);
-  const int trow1 = (8 + 4 * hh + r4) * RB, tsw1 = swz<D>(8 + 4 * hh + r4);
-
-  wait_vmem<0>();
-  __syncthreads();
-  issue(0);
-  for (int step = 0; step < nsteps; ++step) {
-    const int sn = step + 1;
-    const bool new_blk = sn < nsteps && sn % ngrp == 0 && (sn / ngrp) % SPB == 0;
-    if (new_blk && tid < IDX_BLK) {
-      const int blk = (sn / ngrp) / SPB;
-      s_row[blk & 1][tid] = pre_row;
-      s_qpos[blk & 1][tid] = pre_qpos;
-    }
-    wait_vmem<0>();
-    __syncthreads();
-    if (sn < nsteps) {
-      issue(sn);
-      if (new_blk && tid < IDX_BLK) {
-        const int nxt = ((sn / ngrp) / SPB + 1) * IDX_BLK + tid;
-        if (nxt - tid < nq) {
-          pre_row = ql[min(nxt, nq - 1)];
-          pre_qpos = nxt < nq ? a.plan.row_pos[pre_row] : -1;
-        }
-      }
-    }
-
-    const int st = step & 1, sub = step / ngrp;
-    const int nh = min(HPS, G - (step % ngrp) * HPS);
-    if (hp >= nh) continue;                    // wave-uniform: this stage has no head for this wave
-    const uint8_t* Qt = stage_q(st, hp);
-    const uint8_t* dOt = stage_do(st, hp);
-    // S = Q K^T and dP = dO V^T (lane <-> key, element v <-> row 8*(v/4) + 4*hh + v%4)
-    f32x16 S = f32x16{}, dP = f32x16{};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int ch = ((2 * s + hh) ^ asw) << 4;
-      S = mfma(as_bf(ld16(Qt + arow + ch)), as_bf(ld16(s_k + krow + ch)), S);
-      dP = mfma(as_bf(ld16(dOt + arow + ch)), as_bf(ld16(s_v + krow + ch)), dP);
-    }
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const f32x4 L2 = *(const f32x4*)&s_stat[st][hp][0][8 * g4 + 4 * hh];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) S[4 * g4 + e] = fast_exp2(fmaf(S[4 * g4 + e], c, -L2[e]));
-    }
-    const int r0 = Q_SUB * sub;
-    if (r0 + Q_SUB > nq || (r0 < it.mask_hi && r0 + Q_SUB > it.mask_lo)) {   // wave-uniform
-      const int* qp = &s_qpos[(sub / SPB) & 1][(sub % SPB) * Q_SUB];
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int4 q4 = *(const int4*)&qp[8 * g4 + 4 * hh];
-        S[4 * g4 + 0] = kpos > q4.x ? 0.f : S[4 * g4 + 0];
-        S[4 * g4 + 1] = kpos > q4.y ? 0.f : S[4 * g4 + 1];
-        S[4 * g4 + 2] = kpos > q4.z ? 0.f : S[4 * g4 + 2];
-        S[4 * g4 + 3] = kpos > q4.w ? 0.f : S[4 * g4 + 3];
-      }
-    }
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const f32x4 Dl = *(const f32x4*)&s_stat[st][hp][1][8 * g4 + 4 * hh];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) dP[4 * g4 + e] = S[4 * g4 + e] * (dP[4 * g4 + e] - Dl[e]);
-    }
-    const bf16x8 pa0 = pack8(S, 0), pa1 = pack8(S, 8);
-    const bf16x8 sa0 = pack8(dP, 0), sa1 = pack8(dP, 8);
-#pragma unroll
-    for (int nb = 0; nb < DB; ++nb) {
-      // B operands dO^T and Q^T by transposing reads: rows 16t + 8rd + 4hh + r4, column 32nb + l32
-      const int o0 = trow0 + (((4 * nb + tcol) ^ tsw0) << 4) + tbyte;
-      const int o1 = trow1 + (((4 * nb + tcol) ^ tsw1) << 4) + tbyte;
-      dv[nb] = mfma(pa0, as_bf(lds_tr(dOt + o0), lds_tr(dOt + o1)), dv[nb]);
-      dv[nb] = mfma(pa1, as_bf(lds_tr(dOt + 16 * RB + o0), lds_tr(dOt + 16 * RB + o1)), dv[nb]);
-      dk[nb] = mfma(sa0, as_bf(lds_tr(Qt + o0), lds_tr(Qt + o1)), dk[nb]);
-      dk[nb] = mfma(sa1, as_bf(lds_tr(Qt + 16 * RB + o0), lds_tr(Qt + 16 * RB + o1)), dk[nb]);
-    }
-  }
-
-  // fixed-order pair sum: the head-1 wave of each key group parks its partial sums in LDS
-  __syncthreads();
-  float* park = (float*)smem + (size_t)kg * (2 * DB * 16 * 64);
-  if (hp == 1) {
-#pragma unroll
-    for (int nb = 0; nb < DB; ++nb) {
-      *(f32x16*)(park + ((0 * DB + nb) * 64 + lane) * 16) = dk[nb];
-      *(f32x16*)(park + ((1 * DB + nb) * 64 + lane) * 16) = dv[nb];
-    }
-  }
-  __syncthreads();
-  if (hp == 1) return;
-#pragma unroll
-  for (int nb = 0; nb < DB; ++nb) {
-    dk[nb] += *(const f32x16*)(park + ((0 * DB + nb) * 64 + lane) * 16);
-    dv[nb] += *(const f32x16*)(park + ((1 * DB + nb) * 64 + lane) * 16);
-  }
-
-  // accumulator layout: lane <-> head_dim column 32*nb + l32, element v <-> key of this group
-  const float scale = a.s.scale;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int key = 32 * kg + 8 * (v >> 2) + 4 * hh + (v & 3);
-    if (key >= it.nk) continue;
-    float* kdst;
-    float* vdst;
-    if (it.part < 0) {
-      const size_t o = (size_t)s_slot[key] * kv_stride + (size_t)hk * D;
-      kdst = a.dK + o;
-      vdst = a.dV + o;
-    } else {
-      const size_t o = ((size_t)it.part * BKV_TILE + key) * D;
-      kdst = a.part_dk + o;
-      vdst = a.part_dv + o;
-    }
-#pragma unroll
-    for (int nb = 0; nb < DB; ++nb) {
-      kdst[32 * nb + l32] = dk[nb][v] * scale;
-      vdst[32 * nb + l32] = dv[nb][v];
-    }
-  }
-}
-
-template <int D, int NW, int NS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void bwd_dq_bf16_kernel(BwdArgs a) {
-  constexpr int RB = D * 2;
-  constexpr int CPR = D / 8;
-  constexpr int RPI = 64 / CPR;
-  constexpr int TB = KV_TILE * RB;
-  constexpr int NI = KV_TILE / RPI;
-  constexpr int IPW = (NI + NW - 1) / NW;
-  constexpr int KS = D / 16, DB = D / 32;
-  constexpr int TPB = IDX_BLK / KV_TILE;
-  constexpr int CPW = 2 * (NI / NW);          // K+V copies every wave issues per tile (at least)
-  static_assert(NS - 1 <= TPB, "index blocks are fetched once per TPB tiles");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];   // [stage][K | V]
-  __shared__ int s_slot[2][IDX_BLK];
-
-  const FwdItem it = a.plan.fwd[blockIdx.x];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, hh = lane >> 5;
-  const int rw = a.s.rw;
-  const int head = it.head0 + wave / rw;
-  const int hk = it.head0 / a.s.g;
-  const int ridx = (wave % rw) * 32 + l32;
-  const bool row_ok = ridx < it.nq;
-  const int row = a.plan.q_list[it.q_off + (row_ok ? ridx : it.nq - 1)];
-  const int qpos = a.plan.row_pos[row];
-  const float lse2 = a.lse2[(size_t)head * a.s.ns + row];
-  const float del = a.delta[(size_t)head * a.s.ns + row];
-  const int nkv = it.nkv;
-  const int* kvl = a.plan.kv_list + it.kv_off;
-  const int ntiles = (nkv + KV_TILE - 1) / KV_TILE;
-
-  if (tid < IDX_BLK) {
-    s_slot[0][tid] = kvl[min(tid, nkv - 1)];
-    if (nkv > IDX_BLK) s_slot[1][tid] = kvl[min(IDX_BLK + tid, nkv - 1)];
-  }
-
-  bf16x8 qreg[KS], doreg[KS];
-  {
-    const size_t o = ((size_t)row * a.s.hq + head) * D + 8 * hh;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      qreg[s] = as_bf(ld16((const bf16_t*)a.Q + o + 16 * s));
-      doreg[s] = as_bf(ld16((const bf16_t*)a.dO + o + 16 * s));
-    }
-  }
-  int koff[KS];
-#pragma unroll
-  for (int s = 0; s < KS; ++s) koff[s] = tile_off<D>(l32, 2 * s + hh);
-  int toff[2][DB];
-  {
-    const int r4 = (lane & 15) >> 2, j = lane & 3, dsub = 16 * ((lane >> 4) & 1);
-#pragma unroll
-    for (int rd = 0; rd < 2; ++rd)
-#pragma unroll
-      for (int mb = 0; mb < DB; ++mb)
-        toff[rd][mb] = tile_off<D>(8 * rd + 4 * hh + r4, (32 * mb + dsub + 4 * j) >> 3) + 8 * (j & 1);
-  }
-
-  const size_t kv_stride = (size_t)a.s.hkv * D;
-  const bf16_t* Kb = (const bf16_t*)a.K + (size_t)hk * D;
-  const bf16_t* Vb = (const bf16_t*)a.V + (size_t)hk * D;
-  const int crow = lane / CPR, cpc = lane % CPR;
-  auto issue = [&](int t) {
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int k = wave + NW * i;
-      if (NI % NW == 0 || k < NI) {
-        const int r = k * RPI + crow;
-        const int key = min(t * KV_TILE + r, nkv - 1);
-        const int slot = s_slot[(key / IDX_BLK) & 1][key % IDX_BLK];
-        const size_t go = (size_t)slot * kv_stride + ((cpc ^ swz<D>(r)) << 3);
-        copy16_to_lds(Kb + go, &smem[t % NS][0][k * 1024]);
-        copy16_to_lds(Vb + go, &smem[t % NS][1][k * 1024]);
-      }
-    }
-  };
-
-  // index block b (entries IDX_BLK*b ...) into its LDS buffer, one dword per lane
-  auto fetch_index_block = [&](int b) {
-    if (b * IDX_BLK >= nkv) return;
-    for (int w = wave; w < IDX_BLK / 64; w += NW)
-      copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
-  };
-
-  f32x16 dq[DB];
-#pragma unroll
-  for (int mb = 0; mb < DB; ++mb) dq[mb] = f32x16{};
-  const float c = a.s.scale * kLog2e;
-
-  wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
-  __syncthreads();
-  // NS-stage ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed.  Index blocks
-  // (TPB tiles each) are double-buffered in LDS: blocks 0 and 1 are loaded up front, and block
-  // b+1 is copied global -> LDS when tile TPB*b is issued, into the buffer of block b-1, whose
-  // tiles have all been issued by then.  The waits before later tiles cover that copy.
-#pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < ntiles) issue(p);
-  for (int t = 0; t < ntiles; ++t) {
-    const int tn = t + NS - 1;                 // tile issued in this iteration
-    // this wave's copies for tile t are done once at most CPW*(NS-2) newer copies are in flight
-    if (t + NS - 2 < ntiles) wait_vmem<CPW * (NS - 2)>();
-    else wait_vmem<0>();
-    __syncthreads();
-    if (tn < ntiles) {
-      issue(tn);
-      if (tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
-    }
-
-    const uint8_t* Kt = &smem[t % NS][0][0];
-    const uint8_t* Vt = &smem[t % NS][1][0];
-    f32x16 S[2], dP[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      S[b] = f32x16{};
-      dP[b] = f32x16{};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        S[b] = mfma(as_bf(ld16(Kt + 32 * b * RB + koff[s])), qreg[s], S[b]);
-        dP[b] = mfma(as_bf(ld16(Vt + 32 * b * RB + koff[s])), doreg[s], dP[b]);
-      }
-    }
-    // accumulator layout: lane <-> query row (column), element v <-> key 32*b + 8*(v/4) + 4*hh + v%4
-    if (t >= it.nfull) {   // wave-uniform: keys past the range or after the row get probability 0
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kidx = t * KV_TILE + 32 * b + 8 * (v >> 2) + 4 * hh + (v & 3);
-          if (kidx >= nkv || it.kv_pos0 + kidx > qpos) S[b][v] = kNegInf;
-        }
-    }
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) dP[b][v] = fast_exp2(fmaf(S[b][v], c, -lse2)) * (dP[b][v] - del);
-    bf16x8 sb[2][2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      sb[b][0] = pack8(dP[b], 0);
-      sb[b][1] = pack8(dP[b], 8);
-    }
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-        for (int mb = 0; mb < DB; ++mb) {
-          const uint8_t* kp = Kt + (32 * b + 16 * t2) * RB;
-          dq[mb] = mfma(as_bf(lds_tr(kp + toff[0][mb]), lds_tr(kp + toff[1][mb])), sb[b][t2], dq[mb]);
-        }
-  }
-
-  if (!row_ok) return;
-  const float scale = a.s.scale;
-  float* dst = it.part < 0 ? a.dQ + ((size_t)row * a.s.hq + head) * D
-                           : a.part_dq + (((size_t)it.part + ridx) * a.s.hq + head) * D;
-#pragma unroll
-  for (int mb = 0; mb < DB; ++mb)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4)
-      *(f32x4*)(dst + 32 * mb + 8 * g4 + 4 * hh) = f32x4{dq[mb][4 * g4] * scale, dq[mb][4 * g4 + 1] * scale,
-                                                          dq[mb][4 * g4 + 2] * scale, dq[mb][4 * g4 + 3] * scale};
-}
 
 // ============================================================================================
 // bf16 dK/dV kernel, one wavefront per SIMD.  Four wavefronts: wave w owns keys 32w .. 32w+31
@@ -427,7 +49,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // Q, dO and their LSE log2 e and Delta), in a five-deep ring.  Iteration i issues the dV/dK
 // MFMAs of step i-1 (dV += P^T dO, dK += dS^T Q), then the S and dP MFMAs of step i+1, and
 // between them computes P = exp2(S c - LSE log2 e) and dS = P (dP - Delta) of step i.
-template <int D>
+template <int D, bool REM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void bwd_kv_bf16_1w_kernel(BwdArgs a) {
   constexpr int RB = D * 2;
   constexpr int LRB = D == 128 ? 8 : 7;       // log2(RB)
@@ -576,24 +198,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
   // ---- iteration i, NSLOT MFMA slots in NP pairs:
   //   pairs 0 .. NT-1: dV[nb] += P^T dO and dK[nb] += dS^T Q of step i-1 (pair u = DB*t2 + nb)
+  //   (REM) then, on a step where some P > 2^-9 or |dS| > 2^-5: the same products of the
+  //         remainders P - bf16(P) and dS - bf16(dS), from step i-1's fp32 P and dS
   //   pair NT:         S and dP of step i+1 start as -LSE/scale and -Delta (the statistics pair)
   //   then:            S += Q K^T and dP += dO V^T of step i+1 (pair = k-step s)
-  // with P and dS of step i computed between them.  Sc/dPc: step i; Sn/dPn: step i+1 (written);
-  // Pp/Sp: packed P and dS of step i-1; Pc/Sc2: of step i (written).  S and dP thus leave the
-  // MFMAs as S - LSE/scale and dP - Delta: P = exp2(c S') and dS = P dP' take two VALU products.
-  // On a step whose rows may see only part of the tile, the causal mask sets S to -inf at the
-  // start of the iteration that consumes it.
-  // Fragments are read PF pairs ahead of their MFMAs; the last pairs read the first PF dV/dK
-  // fragments of iteration i+1 (step i's rows, long landed), so an iteration never starts with
-  // an empty queue.  After slot BAR (MFMAs in flight) the wave waits for its copies of step i+1,
-  // then a barrier: every wave is past iteration i-1, so step i+1 is in LDS and step i-2's ring
-  // slot is free.  The copies of step i+3 into it follow, three slots apart, then (at a subtile
-  // boundary) the row offsets of the next subtile.  A row block is staged in the iteration that
-  // fetches the rows of its first subtile; the buffer it overwrites last held the block before the
-  // previous one, whose readers (at least SPB*G >= 8 steps earlier) are all past the last barrier.
-  // The loop's bookkeeping is incremental and uniform: the copy step's head, head offsets and
-  // subtile advance by one step per iteration (the rows freeze once the copies pass the last step:
-  // they then refill a slot no one reads).
+  // with P and dS of step i computed between them.  Sc/dPc: step i; Sn/dPn: step i+1 (written
+  // from pair NT on; until then they still hold step i-1's fp32 P and dS); Pp/Sp: packed P and dS
+  // of step i-1; Pc/Sc2: of step i (written).  S and dP thus leave the MFMAs as S - LSE/scale and
+  // dP - Delta: P = exp2(c S') and dS = P dP' take two VALU products.
+  // Why the remainders: dV_j = sum_i P_ij dO_i sums over every consumer of key j.  A single bf16
+  // rounding of P leaves up to 2^-8 relative error per term, and these errors add up like a random
+  // walk, ~2^-8/sqrt(3) * sqrt(sum_i P_ij^2 dO_i^2) at most: on a key that many consumers weight
+  // heavily (a shared prefix token with attention-sink-like scores) that grows without bound.
+  // With P = hi + lo, both bf16, each term is good to ~2^-16.  A step is left single-rounded only
+  // when all its P <= 2^-9 (each term then off by <= 2^-17) and all |dS| <= 2^-5 (<= 2^-13); the
+  // same holds for dS in dK = dS^T Q.  The forward and dQ products sum over keys, whose weights
+  // P_i. add up to 1, and need no remainder terms.
   constexpr int NT = 2 * DB;                  // dV/dK slot pairs
   constexpr int PF = 3;
   constexpr int NP = NT + 1 + KS;             // pairs: dV/dK, statistics, S/dP k-steps
@@ -630,6 +250,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
         for (int k = 0; k < 4; ++k) S[4 * g + k] = kpos > q[k] ? kNegInf : S[4 * g + k];
       }
+    }
+  };
+  // remainder products of one step, if any of its P > 2^-9 or |dS| > 2^-5 (wave-uniform branch):
+  // Pf/Sf its fp32 P and dS, Ph/Sh their packed bf16, Qs/dOs its ring slot
+  constexpr float kRemP = 1.0f / 512, kRemS = 1.0f / 32;
+  auto remainders = [&](const f32x16& Pf, const f32x16& Sf, const bf16x8 (&Ph)[2], const bf16x8 (&Sh)[2], uint32_t Qs,
+                        uint32_t dOs) __attribute__((always_inline)) {
+    float mp = max3f(Pf[0], Pf[1], Pf[2]), ms = max3abs(0.f, Sf[0], Sf[1]);
+#pragma unroll
+    for (int v = 3; v < 15; v += 2) mp = max3f(mp, Pf[v], Pf[v + 1]);
+    mp = max2f(mp, Pf[15]);
+#pragma unroll
+    for (int v = 2; v < 16; v += 2) ms = max3abs(ms, Sf[v], Sf[v + 1]);
+    if (__builtin_amdgcn_ballot_w64(mp > kRemP || ms > kRemS) == 0) return;
+    bf16x8 pl[2], sl[2];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      pl[t2] = pack8_rem(Pf, 8 * t2, Ph[t2]);
+      sl[t2] = pack8_rem(Sf, 8 * t2, Sh[t2]);
+      anchor(pl[t2]);   // written before the fence, not next to an MFMA
+      anchor(sl[t2]);
+    }
+    valu_fence();
+#pragma unroll
+    for (int u = 0; u < NT; ++u) {
+      const int t2 = u / DB, nb = u % DB;
+      mma_a(dv[nb], pl[t2], ld_t(dOs, u));
+      mma_a(dk[nb], sl[t2], ld_t(Qs, u));
     }
   };
   int h3, subc;                               // head of the copy step i+3 and subtile of min(i+3, nsteps-1)
@@ -700,12 +348,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           anchor(Pc[v / 8]);
           anchor(Sc2[v / 8]);
         }
+
       });
     };
     auto slot = [&](auto ic) __attribute__((always_inline)) {
       constexpr int si = decltype(ic)::value;
       constexpr int m = si / 2, w = si % 2;
       if constexpr (si == 0) mask_s(Sc, i, sub0);
+      if constexpr (REM && si == 2 * NT) {   // before the statistics pair overwrites Sn / dPn
+        remainders(Sn, dPn, Pp, Sp, Qp, dOp);
+        sched_fence();
+      }
       if constexpr (w == 0) load_frag(m + PF);
       if constexpr (m < NT) {
         constexpr int t2 = m / DB, nb = m % DB;
@@ -808,6 +461,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       anchor(PB[t2]);   // the zeros are written here, before the fence, not next to an MFMA
       anchor(DSB[t2]);
     }
+    // step -1's fp32 P and dS (read by iteration 0's remainder test) are zero
+    SB = dPB = f32x16{};
+    anchor(SB);
+    anchor(dPB);
     mfma_fence();
   }
 
@@ -847,12 +504,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         mma_a(dk[nb], Sl[t2], tk);
       }
     };
-    // one code path: the last step's P and dS are moved into the even buffers first
+    // one code path: the last step's P and dS (packed, and in fp32 for the remainders) are moved
+    // into the even buffers first
     if (odd_last) {
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2) {
         PA[t2] = PB[t2];
         DSA[t2] = DSB[t2];
+      }
+      if constexpr (REM) {
+        SA = SB;
+        dPA = dPB;
       }
     }
 #pragma unroll
@@ -862,6 +524,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
     valu_fence();
     last(PA, DSA);
+    if constexpr (REM) remainders(SA, dPA, PA, DSA, Ql, dOl);
     mfma_fence();
 #pragma unroll
     for (int nb = 0; nb < DB; ++nb) {
@@ -939,6 +602,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
   int ridx[NH], row[NH], lim[NH];
   bool row_ok[NH];
   float lse2[NH], del[NH];
+  // sum over this lane's keys of dS' = P (dP - Delta), with Delta = dO . O from the bf16 O: the
+  // row's total is Delta' - Delta, so that the dK/dV pass can use the exact Delta' = sum_j P dP
+  float eps[NH];
   bf16x8 qreg[NH][KS], doreg[NH][KS];
 #pragma unroll
   for (int rh = 0; rh < NH; ++rh) {
@@ -961,7 +627,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
   const bf16x8 ones_k01 = as_bf(hh ? u32x4{0u, 0u, 0u, 0u} : u32x4{0x3F803F80u, 0u, 0u, 0u});
   bf16x8 ndel[NH];
 #pragma unroll
-  for (int rh = 0; rh < NH; ++rh) ndel[rh] = as_bf(u32x4{hh ? 0u : split_bf16(-del[rh]), 0u, 0u, 0u});
+  for (int rh = 0; rh < NH; ++rh) {
+    ndel[rh] = as_bf(u32x4{hh ? 0u : split_bf16(-del[rh]), 0u, 0u, 0u});
+    eps[rh] = 0.f;
+  }
   // LDS byte offsets of this lane's fragments inside a 32-key block (gtile_off layout): K or V
   // fragment s (rows l32, chunk 2s + hh) at koff[s & 1] + 1024 (s >> 1); K^T fragment of k-step
   // t2 and d block mb (rows 16 t2 + 8 rd + 4 hh + r4, chunks 4 mb + (dsub + 4 j) / 8) at
@@ -1052,7 +721,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
           Sc[rh][v] = fmaf(Sc[rh][v], c, -lse2[rh]);
         }
         if constexpr (F(e) + 1 == q) Sc[rh][v] = fast_exp2(Sc[rh][v]);
-        if constexpr (F(e) + 2 == q) dPc[rh][v] = Sc[rh][v] * dPc[rh][v];
+        if constexpr (F(e) + 2 == q) {
+          dPc[rh][v] = Sc[rh][v] * dPc[rh][v];
+          eps[rh] += dPc[rh][v];
+        }
         if constexpr (v % 8 == 7 && F(e) + 2 == q) {
           dSc[rh][v / 8] = pack8(dPc[rh], 8 * (v / 8));
           anchor(dSc[rh][v / 8]);
@@ -1207,6 +879,22 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
     for (int rh = 0; rh < NH; ++rh)
 #pragma unroll
       for (int mb = 0; mb < DB; ++mb) pin_a(dq[rh][mb]);
+  }
+  // the exact Delta' = Delta + (row sum of dS'), as the (hi, lo) bf16 start value -Delta' of the
+  // dK/dV kernel's dP accumulators; a row whose key range was split leaves its part of the sum to
+  // the fixed-order reduction of the pieces
+#pragma unroll
+  for (int rh = 0; rh < NH; ++rh) {
+    const float e = pair_sum(eps[rh]);   // lanes l and l ^ 32 hold different keys of one row
+    if (hh == 0 && row_ok[rh]) {
+      if (it.part < 0) {
+        const uint32_t w = split_bf16(-del[rh]);
+        const float d0 = bf2f(w & 0xffffu) + bf2f(w >> 16);   // the -Delta the dP products started from
+        ((uint32_t*)a.kv_nd)[(size_t)head * a.s.ns + row[rh]] = split_bf16(d0 - e);
+      } else {
+        a.part_eps[((size_t)it.part + ridx[rh]) * a.s.hq + head] = e;
+      }
+    }
   }
 
   // dQ rows leave as whole fp32 rows: each wave stages one 32-row half at a time in its own part of
@@ -1502,11 +1190,23 @@ __global__ __launch_bounds__(256) void bwd_reduce_kv_kernel(BwdArgs a) {
   }
 }
 
-// dQ = sum of partial rows in ascending piece order
+// dQ = sum of partial rows in ascending piece order (bf16: also the pieces' row sums of dS', which
+// complete the exact Delta' of the dK/dV kernel, as the dQ kernel does for unsplit rows)
+template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_reduce_dq_kernel(BwdArgs a) {
   const MergeEntry e = a.plan.merge[blockIdx.x];
   const int D = a.s.d, hq = a.s.hq, bmq = a.s.bmq;
   const int per_row = hq * D / 4;
+  if (BF16) {
+    for (int idx = blockIdx.y * blockDim.x + threadIdx.x; idx < e.nq * hq; idx += gridDim.y * blockDim.x) {
+      const int i = idx / hq, h = idx % hq;
+      float s = 0.f;
+      for (int j = 0; j < e.nparts; ++j) s += a.part_eps[((size_t)e.part0 + (size_t)j * bmq + i) * hq + h];
+      uint32_t* nd = (uint32_t*)a.kv_nd + (size_t)h * a.s.ns + a.plan.q_list[e.q_off + i];
+      const uint32_t w = *nd;
+      *nd = split_bf16(bf2f(w & 0xffffu) + bf2f(w >> 16) - s);
+    }
+  }
   for (int idx = blockIdx.y * blockDim.x + threadIdx.x; idx < e.nq * per_row; idx += gridDim.y * blockDim.x) {
     const int i = idx / per_row, r = (idx % per_row) * 4;
     f32x4 acc = f32x4{};
@@ -1531,16 +1231,6 @@ __global__ __launch_bounds__(256) void bwd_zero_pad_kernel(BwdArgs a) {
 
 }  // namespace
 
-#define PSATTN_NW_SWITCH(NW, BODY)                  \
-  switch (NW) {                                     \
-    case 4: { constexpr int W_ = 4; BODY; } break;  \
-    case 5: { constexpr int W_ = 5; BODY; } break;  \
-    case 6: { constexpr int W_ = 6; BODY; } break;  \
-    case 7: { constexpr int W_ = 7; BODY; } break;  \
-    case 8: { constexpr int W_ = 8; BODY; } break;  \
-    default: return hipErrorInvalidValue;           \
-  }
-
 hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st) {
   const int rows_per_block = 256 / (a.s.d / 8) * PRE_PASSES;
   const int64_t blocks_per_head = ((int64_t)a.s.ns + rows_per_block - 1) / rows_per_block;
@@ -1551,19 +1241,12 @@ hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st) {
 }
 
 hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st) {
+  // (the bf16 kernel addresses the pools and the Q / dO tensors by 32-bit byte offsets; the host
+  // rejects larger trees with PSATTN_E_UNSUPPORTED)
   const dim3 grid(a.n_bkv), block(256);
   if (bf16) {
-    // one wavefront per SIMD: pools and the Q / dO tensors addressed by 32-bit byte offsets
-    const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
-    const int64_t q_bytes = (int64_t)a.s.ns * a.s.hq * a.s.d * 2;
-    if (a.pool_slots <= (1 << 24) && a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX &&
-        q_bytes <= (int64_t)UINT32_MAX && (int64_t)a.s.ns * a.s.hq < (1 << 24)) {
-      if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_1w_kernel<128>), grid, block, 0, st, a);
-      else hipLaunchKernelGGL((bwd_kv_bf16_1w_kernel<64>), grid, block, 0, st, a);
-      return hipGetLastError();
-    }
-    if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_kernel<128>), grid, dim3(512), 0, st, a);
-    else hipLaunchKernelGGL((bwd_kv_bf16_kernel<64>), grid, dim3(512), 0, st, a);
+    if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_bf16_1w_kernel<128, PSATTN_KV_REM>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((bwd_kv_bf16_1w_kernel<64, PSATTN_KV_REM>), grid, block, 0, st, a);
   } else {
     if (a.s.d == 128) hipLaunchKernelGGL((bwd_kv_f32_kernel<128>), grid, block, 0, st, a);
     else hipLaunchKernelGGL((bwd_kv_f32_kernel<64>), grid, block, 0, st, a);
@@ -1574,21 +1257,12 @@ hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st) {
 hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_fwd);
   if (bf16) {
-    const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
-    if (a.s.rw % PSATTN_DQ_NH == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
-        a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 8 / NH waves of NH*32 rows
-      constexpr int NW = 8 / PSATTN_DQ_NH;
-      const dim3 block(NW * 64);
-      if (a.s.d == 128) hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<128, NW, 4, PSATTN_DQ_NH>), grid, block, 0, st, a);
-      else hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<64, NW, 4, PSATTN_DQ_NH>), grid, block, 0, st, a);
-      return hipGetLastError();
-    }
-    const dim3 block(a.s.nw * 64);
-    if (a.s.d == 128) {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<128, W_, 2>), grid, block, 0, st, a));
-    } else {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, W_, 2>), grid, block, 0, st, a));
-    }
+    // 8 / NH waves of NH*32 rows (the planner makes every item 8 (subtile, head) pairs)
+    if (a.s.rw % PSATTN_DQ_NH != 0 || a.s.nw != 8) return hipErrorInvalidValue;
+    constexpr int NW = 8 / PSATTN_DQ_NH;
+    const dim3 block(NW * 64);
+    if (a.s.d == 128) hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<128, NW, 4, PSATTN_DQ_NH>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((bwd_dq_bf16_w64_kernel<64, NW, 4, PSATTN_DQ_NH>), grid, block, 0, st, a);
   } else {
     const dim3 block(2 * a.s.bmq * a.s.hc);
     if (a.s.d == 128) hipLaunchKernelGGL((bwd_dq_f32_kernel<128>), grid, block, 0, st, a);
@@ -1602,8 +1276,9 @@ hipError_t launch_bwd_reduce_kv(const BwdArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_reduce_dq(const BwdArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(bwd_reduce_dq_kernel, dim3(a.n_merge, kMergeSlices), dim3(256), 0, st, a);
+hipError_t launch_bwd_reduce_dq(const BwdArgs& a, bool bf16, hipStream_t st) {
+  if (bf16) hipLaunchKernelGGL(bwd_reduce_dq_kernel<true>, dim3(a.n_merge, kMergeSlices), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL(bwd_reduce_dq_kernel<false>, dim3(a.n_merge, kMergeSlices), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -75,6 +75,18 @@ __device__ __forceinline__ bf16x8 pack8(const f32x16& x, int base) {
   return as_bf(w);
 }
 
+// The remainders x - hi of the same 8 values, given hi = pack8(x, base): one bf16x8 operand that,
+// added to hi in a product, carries x to ~2^-17 relative (hi's element 2k sits in the low half of
+// dword k, element 2k+1 in the high half)
+__device__ __forceinline__ bf16x8 pack8_rem(const f32x16& x, int base, const bf16x8& hi) {
+  const u32x4 h = __builtin_bit_cast(u32x4, hi);
+  u32x4 w;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    w[k] = pack2(x[base + 2 * k] - __uint_as_float(h[k] << 16), x[base + 2 * k + 1] - __uint_as_float(h[k] & 0xffff0000u));
+  return as_bf(w);
+}
+
 // Max / sum over the lane pair (l, l ^ 32) with one v_permlane32_swap: whichever half the
 // instruction exchanges, the two results hold this lane's value and its partner's.
 __device__ __forceinline__ float pair_max(float x) {
@@ -93,10 +105,6 @@ template <int D>
 __device__ __forceinline__ int swz(int r) {
   if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
   else return (r >> 1) & 7;
-}
-template <int D>
-__device__ __forceinline__ int tile_off(int r, int c) {
-  return r * (D * 2) + ((c ^ swz<D>(r)) << 4);
 }
 
 // ---- LDS tiles of the one-wavefront-per-SIMD kernels (rows of D bf16).  Rows come in groups
@@ -215,6 +223,11 @@ __device__ __forceinline__ void valu_fence() { asm volatile("s_nop 1"); }
 __device__ __forceinline__ float max3f(float a, float b, float c) {
   float r;
   asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float max3abs(float a, float b, float c) {   // max(a, |b|, |c|)
+  float r;
+  asm("v_max3_f32 %0, %1, |%2|, |%3|" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
 }
 __device__ __forceinline__ float max2f(float a, float b) {

@@ -9,11 +9,9 @@
 //
 // Key tiles (64 keys) are gathered through the path's slot list, one row per key, and copied
 // global -> LDS directly (global_load_lds_dwordx4) into a ring while earlier tiles are computed:
-// a 4-stage ring in the grouped layout of gtile_off for the main kernel (fwd_bf16_w64_kernel,
-// NH 32-row halves per wave), a 2-stage ring of swizzled rows for the older multi-wave kernel
-// (fwd_bf16_kernel, one 32-row subtile per wave; used where the main kernel's 32-bit offsets
-// do not reach).  The running max is only moved when it grows by more than 2^8, so O and the
-// row sum are rarely rescaled.
+// a 4-stage ring in the grouped layout of gtile_off (fwd_bf16_w64_kernel, NH 32-row halves per
+// wave).  The running max is only moved when it grows by more than 2^8, so O and the row sum
+// are rarely rescaled.
 #include "psattn_device.h"
 
 #ifndef PSATTN_FWD_NS
@@ -33,207 +31,6 @@ namespace psattn {
 namespace {
 
 using namespace dev;
-
-template <int D, int NW, int NS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_bf16_kernel(FwdArgs a) {
-  constexpr int RB = D * 2;                      // bytes per tile row
-  constexpr int CPR = D / 8;                     // 16-byte chunks per row
-  constexpr int RPI = 64 / CPR;                  // rows per 64-lane copy instruction
-  constexpr int TB = KV_TILE * RB;               // bytes per K or V tile
-  constexpr int NI = KV_TILE / RPI;              // copy instructions per tile and tensor
-  constexpr int IPW = (NI + NW - 1) / NW;
-  constexpr int KS = D / 16;                     // k-steps over head_dim
-  constexpr int DB = D / 32;                     // 32-wide head_dim blocks of O
-  constexpr int TPB = IDX_BLK / KV_TILE;         // key tiles per staged index block
-  constexpr int CPW = 2 * (NI / NW);          // K+V copies every wave issues per tile (at least)
-  static_assert(NS - 1 <= TPB, "index blocks are fetched once per TPB tiles");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][2][TB];   // [stage][K | V]
-  __shared__ int s_slot[2][IDX_BLK];
-
-  const FwdItem it = a.plan.fwd[blockIdx.x];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, hh = lane >> 5;
-  const int rw = a.s.rw;
-  const int head = it.head0 + wave / rw;
-  const int hk = it.head0 / a.s.g;
-  const int ridx = (wave % rw) * 32 + l32;
-  const bool row_ok = ridx < it.nq;
-  const int row = a.plan.q_list[it.q_off + (row_ok ? ridx : it.nq - 1)];
-  const int qpos = a.plan.row_pos[row];
-  const int nkv = it.nkv;
-  const int* kvl = a.plan.kv_list + it.kv_off;
-  const int ntiles = (nkv + KV_TILE - 1) / KV_TILE;
-
-  if (tid < IDX_BLK) {
-    s_slot[0][tid] = kvl[min(tid, nkv - 1)];
-    if (nkv > IDX_BLK) s_slot[1][tid] = kvl[min(IDX_BLK + tid, nkv - 1)];
-  }
-
-  bf16x8 qreg[KS];
-  {
-    const bf16_t* qp = (const bf16_t*)a.Q + ((size_t)row * a.s.hq + head) * D + 8 * hh;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qreg[s] = as_bf(ld16(qp + 16 * s));
-  }
-
-  // LDS read offsets of this lane (independent of the tile and of the 32-row block)
-  int koff[KS];          // row-major A operand: row l32, chunk 2s + hh
-#pragma unroll
-  for (int s = 0; s < KS; ++s) koff[s] = tile_off<D>(l32, 2 * s + hh);
-  int voff[2][DB];       // transposing reads: rows 8rd + 4hh + r4, columns 32mb + dsub + 4j
-  {
-    const int r4 = (lane & 15) >> 2, j = lane & 3, dsub = 16 * ((lane >> 4) & 1);
-#pragma unroll
-    for (int rd = 0; rd < 2; ++rd)
-#pragma unroll
-      for (int mb = 0; mb < DB; ++mb)
-        voff[rd][mb] = tile_off<D>(8 * rd + 4 * hh + r4, (32 * mb + dsub + 4 * j) >> 3) + 8 * (j & 1);
-  }
-
-  const size_t kv_stride = (size_t)a.s.hkv * D;
-  const bf16_t* Kb = (const bf16_t*)a.K + (size_t)hk * D;
-  const bf16_t* Vb = (const bf16_t*)a.V + (size_t)hk * D;
-  const int crow = lane / CPR, cpc = lane % CPR;
-  auto issue = [&](int t) {
-    uint8_t* kdst = &smem[t % NS][0][0];
-    uint8_t* vdst = &smem[t % NS][1][0];
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int k = wave + NW * i;
-      if (NI % NW == 0 || k < NI) {
-        const int r = k * RPI + crow;
-        const int key = min(t * KV_TILE + r, nkv - 1);
-        const int slot = s_slot[(key / IDX_BLK) & 1][key % IDX_BLK];
-        const size_t go = (size_t)slot * kv_stride + ((cpc ^ swz<D>(r)) << 3);
-        copy16_to_lds(Kb + go, kdst + k * 1024);
-        copy16_to_lds(Vb + go, vdst + k * 1024);
-      }
-    }
-  };
-
-  // index block b (entries IDX_BLK*b ...) into its LDS buffer, one dword per lane
-  auto fetch_index_block = [&](int b) {
-    if (b * IDX_BLK >= nkv) return;
-    for (int w = wave; w < IDX_BLK / 64; w += NW)
-      copy4_to_lds(kvl + min(b * IDX_BLK + 64 * w + lane, nkv - 1), &s_slot[b & 1][64 * w]);
-  };
-
-  f32x16 oacc[DB];
-#pragma unroll
-  for (int mb = 0; mb < DB; ++mb) oacc[mb] = f32x16{};
-  float m_run = kNegInf, l_run = 0.f;
-  const float c = a.s.scale * kLog2e;
-  const float th = 8.f / c;   // max growth (raw score units) tolerated before rescaling
-
-  wait_vmem<0>();   // operands and index block loaded; nothing older stays in flight in the loop
-  __syncthreads();
-  // NS-stage ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed.  Index blocks
-  // (TPB tiles each) are double-buffered in LDS: blocks 0 and 1 are loaded up front, and block
-  // b+1 is copied global -> LDS when tile TPB*b is issued, into the buffer of block b-1, whose
-  // tiles have all been issued by then.  The waits before later tiles cover that copy.
-#pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < ntiles) issue(p);
-  for (int t = 0; t < ntiles; ++t) {
-    const int tn = t + NS - 1;                 // tile issued in this iteration
-    // this wave's copies for tile t are done once at most CPW*(NS-2) newer copies are in flight
-    if (t + NS - 2 < ntiles) wait_vmem<CPW * (NS - 2)>();
-    else wait_vmem<0>();
-    __syncthreads();
-    if (tn < ntiles) {
-      issue(tn);
-      if (tn % TPB == 0 && tn >= TPB) fetch_index_block(tn / TPB + 1);
-    }
-
-    const uint8_t* Kt = &smem[t % NS][0][0];
-    const uint8_t* Vt = &smem[t % NS][1][0];
-    f32x16 sacc[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      sacc[b] = f32x16{};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) sacc[b] = mfma(as_bf(ld16(Kt + 32 * b * RB + koff[s])), qreg[s], sacc[b]);
-    }
-    if (t >= it.nfull) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kidx = t * KV_TILE + 32 * b + 8 * (v >> 2) + 4 * hh + (v & 3);
-          if (kidx >= nkv || it.kv_pos0 + kidx > qpos) sacc[b][v] = kNegInf;
-        }
-    }
-    float mt = kNegInf;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b][v]);
-    mt = pair_max(mt);
-    if (__any(mt > m_run + th)) {
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = m_new == kNegInf ? 1.f : fast_exp2((m_run - m_new) * c);
-      l_run *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < DB; ++mb) oacc[mb] *= alpha;
-      m_run = m_new;
-    }
-    const float mc = m_run == kNegInf ? 0.f : m_run * c;
-    float psum = 0.f;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = fast_exp2(fmaf(sacc[b][v], c, -mc));
-        sacc[b][v] = p;
-        psum += p;
-      }
-    l_run += psum;
-
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      pb[b][0] = pack8(sacc[b], 0);
-      pb[b][1] = pack8(sacc[b], 8);
-    }
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-        for (int mb = 0; mb < DB; ++mb) {
-          const uint8_t* vp = Vt + (32 * b + 16 * t2) * RB;
-          oacc[mb] = mfma(as_bf(lds_tr(vp + voff[0][mb]), lds_tr(vp + voff[1][mb])), pb[b][t2], oacc[mb]);
-        }
-  }
-
-  const float l_tot = pair_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse = l_tot > 0.f ? m_run * a.s.scale + logf(l_tot) : kNegInf;
-  if (!row_ok) return;
-  if (it.part < 0) {
-    bf16_t* op = (bf16_t*)a.O + ((size_t)row * a.s.hq + head) * D;
-#pragma unroll
-    for (int mb = 0; mb < DB; ++mb)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        u32x2 w;
-        w[0] = pack2(oacc[mb][4 * g4 + 0] * inv, oacc[mb][4 * g4 + 1] * inv);
-        w[1] = pack2(oacc[mb][4 * g4 + 2] * inv, oacc[mb][4 * g4 + 3] * inv);
-        *(u32x2*)(op + 32 * mb + 8 * g4 + 4 * hh) = w;
-      }
-    if (hh == 0) a.LSE[(size_t)head * a.s.ns + row] = lse;
-  } else {
-    const size_t prow = (size_t)it.part + ridx;
-    float* op = a.part_o + (prow * a.s.hq + head) * D;
-#pragma unroll
-    for (int mb = 0; mb < DB; ++mb)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4)
-        *(f32x4*)(op + 32 * mb + 8 * g4 + 4 * hh) =
-            f32x4{oacc[mb][4 * g4] * inv, oacc[mb][4 * g4 + 1] * inv, oacc[mb][4 * g4 + 2] * inv, oacc[mb][4 * g4 + 3] * inv};
-    if (hh == 0) a.part_lse[prow * a.s.hq + head] = lse;
-  }
-}
 
 // ============================================================================================
 // bf16 main kernel.  A wavefront holds the queries (AGPRs), the output accumulators (AGPRs) and
@@ -779,33 +576,15 @@ __global__ __launch_bounds__(256) void fwd_merge_kernel(FwdArgs a) {
 
 }  // namespace
 
-#define PSATTN_NW_SWITCH(NW, BODY)                  \
-  switch (NW) {                                     \
-    case 4: { constexpr int W_ = 4; BODY; } break;  \
-    case 5: { constexpr int W_ = 5; BODY; } break;  \
-    case 6: { constexpr int W_ = 6; BODY; } break;  \
-    case 7: { constexpr int W_ = 7; BODY; } break;  \
-    case 8: { constexpr int W_ = 8; BODY; } break;  \
-    default: return hipErrorInvalidValue;           \
-  }
-
 hipError_t launch_fwd_main(const FwdArgs& a, bool bf16, hipStream_t st) {
   const dim3 grid(a.n_items);
   if (bf16) {
-    const int64_t kv_row_bytes = (int64_t)a.s.hkv * a.s.d * 2;
-    if (a.s.rw % PSATTN_FWD_NH == 0 && a.s.nw == 8 && a.pool_slots <= (1 << 24) &&
-        a.pool_slots * kv_row_bytes <= (int64_t)UINT32_MAX) {   // 4 waves of 64 rows
-      const dim3 block(8 / PSATTN_FWD_NH * 64);
-      if (a.s.d == 128) hipLaunchKernelGGL((fwd_bf16_w64_kernel<128, 8 / PSATTN_FWD_NH, PSATTN_FWD_NS, PSATTN_FWD_NH>), grid, block, 0, st, a);
-      else hipLaunchKernelGGL((fwd_bf16_w64_kernel<64, 8 / PSATTN_FWD_NH, PSATTN_FWD_NS, PSATTN_FWD_NH>), grid, block, 0, st, a);
-      return hipGetLastError();
-    }
-    const dim3 block(a.s.nw * 64);
-    if (a.s.d == 128) {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<128, W_, 2>), grid, block, 0, st, a));
-    } else {
-      PSATTN_NW_SWITCH(a.s.nw, hipLaunchKernelGGL((fwd_bf16_kernel<64, W_, 2>), grid, block, 0, st, a));
-    }
+    // 8 / NH waves of NH*32 rows (the planner makes every item 8 (subtile, head) pairs); the pools
+    // are addressed by 32-bit byte offsets (the host rejects larger trees)
+    if (a.s.rw % PSATTN_FWD_NH != 0 || a.s.nw != 8) return hipErrorInvalidValue;
+    const dim3 block(8 / PSATTN_FWD_NH * 64);
+    if (a.s.d == 128) hipLaunchKernelGGL((fwd_bf16_w64_kernel<128, 8 / PSATTN_FWD_NH, PSATTN_FWD_NS, PSATTN_FWD_NH>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((fwd_bf16_w64_kernel<64, 8 / PSATTN_FWD_NH, PSATTN_FWD_NS, PSATTN_FWD_NH>), grid, block, 0, st, a);
   } else {
     const dim3 block(2 * a.s.bmq * a.s.hc);  // two lanes per (row, head)
     if (a.s.d == 128) hipLaunchKernelGGL((fwd_f32_kernel<128>), grid, block, 0, st, a);

@@ -121,6 +121,17 @@ psattn_status validate_and_copy(const psattn_tree_desc* d, psattn_tree* t) {
   }
   if (ns > INT32_MAX / 2) return fail(PSATTN_E_UNSUPPORTED, "too many rows (%lld)", (long long)ns);
   t->Ns = ns;
+  if (t->dtype == PSATTN_BF16) {
+    // the bf16 kernels address the K/V pools and the Q / O / dO tensors by 32-bit byte offsets
+    // and pool slots by 24-bit products
+    const int64_t kv_bytes = t->pool_slots * t->hkv * t->d * 2, q_bytes = ns * t->hq * t->d * 2;
+    if (t->pool_slots > (1 << 24) || kv_bytes > (int64_t)UINT32_MAX)
+      return fail(PSATTN_E_UNSUPPORTED, "bf16 pool of %lld slots (%lld bytes per tensor): at most 2^24 slots and 4 GiB",
+                  (long long)t->pool_slots, (long long)kv_bytes);
+    if (q_bytes > (int64_t)UINT32_MAX || ns * t->hq >= (1 << 24))
+      return fail(PSATTN_E_UNSUPPORTED, "bf16 query tensor of %lld rows x %d heads: at most 4 GiB and 2^24 row-heads",
+                  (long long)ns, t->hq);
+  }
 
   // row ranges tile [0, Ns)
   {
@@ -364,8 +375,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       for (int a = a0; a < a1; ++a) t->q_list.push_back((int32_t)(t->row_off[n] + a));
       int64_t nkv_total = t->off[n] + a1;
       int64_t min_qpos = t->off[n] + a0;
-      int npieces = (int)((nkv_total + split_keys - 1) / split_keys);
-      if (split_keys == INT64_MAX) npieces = 1;
+      const int npieces = split_keys == INT64_MAX ? 1 : (int)((nkv_total + split_keys - 1) / split_keys);
       int32_t part0 = -1;
       if (npieces > 1) {
         part0 = (int32_t)part_rows;
@@ -567,7 +577,7 @@ FwdWs fwd_ws(const psattn_tree* t) {
   w.total = t->fwd_part_rows ? cur : 0;
   return w;
 }
-struct BwdWs { size_t o_delta, o_lse2, o_kv_nls, o_kv_nd, o_part_dq, o_part_dk, o_part_dv, total; };
+struct BwdWs { size_t o_delta, o_lse2, o_kv_nls, o_kv_nd, o_part_dq, o_part_eps, o_part_dk, o_part_dv, total; };
 BwdWs bwd_ws(const psattn_tree* t) {
   BwdWs w;
   size_t cur = 0;
@@ -581,6 +591,8 @@ BwdWs bwd_ws(const psattn_tree* t) {
   cur = align_up(cur + (size_t)t->Ns * t->hq * 4);
   w.o_part_dq = cur;
   cur = align_up(cur + (size_t)t->fwd_part_rows * t->hq * t->d * 4);
+  w.o_part_eps = cur;
+  cur = align_up(cur + (size_t)t->fwd_part_rows * t->hq * 4);
   w.o_part_dk = cur;
   cur = align_up(cur + (size_t)t->bkv_part_tiles * BKV_TILE * t->d * 4);
   w.o_part_dv = cur;
@@ -769,15 +781,18 @@ psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, con
   a.kv_nls = (float*)(wb + w.o_kv_nls);
   a.kv_nd = (float*)(wb + w.o_kv_nd);
   a.part_dq = (float*)(wb + w.o_part_dq);
+  a.part_eps = (float*)(wb + w.o_part_eps);
   a.part_dk = (float*)(wb + w.o_part_dk);
   a.part_dv = (float*)(wb + w.o_part_dv);
   a.pool_slots = t->pool_slots;
   const bool bf16 = t->dtype == PSATTN_BF16;
+  // dQ first: in bf16 mode it also turns Delta (from the bf16 O) into the exact sum_j P dP that the
+  // dK/dV pass uses
   psattn_status s = timed(2, st, [&] { return launch_bwd_pre(a, bf16, st); });
-  if (s == PSATTN_OK) s = timed(3, st, [&] { return launch_bwd_kv(a, bf16, st); });
   if (s == PSATTN_OK) s = timed(4, st, [&] { return launch_bwd_dq(a, bf16, st); });
+  if (s == PSATTN_OK && a.n_merge) s = timed(6, st, [&] { return launch_bwd_reduce_dq(a, bf16, st); });
+  if (s == PSATTN_OK) s = timed(3, st, [&] { return launch_bwd_kv(a, bf16, st); });
   if (s == PSATTN_OK && a.n_reduce) s = timed(5, st, [&] { return launch_bwd_reduce_kv(a, st); });
-  if (s == PSATTN_OK && a.n_merge) s = timed(6, st, [&] { return launch_bwd_reduce_dq(a, st); });
   if (s == PSATTN_OK && a.n_pad) s = timed(7, st, [&] { return launch_bwd_zero_pad(a, st); });
   return s;
 }

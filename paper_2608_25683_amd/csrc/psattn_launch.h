@@ -1,4 +1,4 @@
-// Kernel launchers (defined in psattn_kernels.hip, called by the C ABI).
+// Kernel launchers (defined in psattn_fwd.hip and psattn_bwd.hip, called by the C ABI).
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -36,8 +36,10 @@ struct BwdArgs {
   float* delta;    // [Hq][Ns]
   float* lse2;     // [Hq][Ns] LSE * log2(e)
   float* kv_nls;   // [Hq][Ns] -LSE / scale   (start of the dK/dV kernels' S accumulators)
-  float* kv_nd;    // [Hq][Ns] -Delta         (start of their dP accumulators)
+  float* kv_nd;    // [Hq][Ns] -Delta         (start of their dP accumulators; bf16: the exact
+                   //                          Delta' from the dQ pass, which runs first)
   float* part_dq;  // [partial rows][Hq][d]
+  float* part_eps; // [partial rows][Hq] row sums of dS' of each piece (bf16)
   float* part_dk;  // [partial tiles][BKV_TILE][d]; each tile belongs to one kv head
   float* part_dv;
   int64_t pool_slots;  // rows of the K and V pools
@@ -50,7 +52,7 @@ hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_bwd_kv(const BwdArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_bwd_reduce_kv(const BwdArgs& a, hipStream_t st);
-hipError_t launch_bwd_reduce_dq(const BwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_reduce_dq(const BwdArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_bwd_zero_pad(const BwdArgs& a, hipStream_t st);
 
 }  // namespace psattn

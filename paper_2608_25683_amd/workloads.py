@@ -425,6 +425,22 @@ def make(name: str, tensors: bool = True) -> Workload:
     return wl
 
 
+def add_attention_sink(wl: Workload, key_rows: Sequence[int], logit: float) -> Workload:
+    """Attention-sink inputs: add to every query of every head h a multiple of the key of each
+    row in ``key_rows`` (kv head h // G), so that scale * q . k of that key grows by ``logit``
+    (about log(visible keys) puts half of a row's softmax weight on it).  Q is rounded to the
+    workload dtype again; K, V and dO are unchanged.  Only the inputs change.
+    """
+    G = wl.hq // wl.hkv
+    Q = wl.Q.astype(np.float64)
+    for j in key_rows:
+        for h in range(wl.hq):
+            k = wl.K[int(j), h // G].astype(np.float64)
+            Q[:, h] += (logit / wl.scale) * k / float(k @ k)
+    wl.Q = _round(Q, wl.dtype)
+    return wl
+
+
 def scatter_pool(tree: Tree, K: np.ndarray, V: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
     """Place node-packed K/V rows into the page pool; pad slots get the sentinel."""
     hkv, d = K.shape[1], K.shape[2]

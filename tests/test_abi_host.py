@@ -84,12 +84,30 @@ def test_valid_descriptor_is_accepted(base):
     (lambda d: d.__setitem__("head_dim", 96), "PSATTN_E_UNSUPPORTED"),
     (lambda d: d.__setitem__("softmax_scale", float("nan")), "PSATTN_E_INVALID_ARG"),
     (lambda d: d.__setitem__("pool_slots", 0), "PSATTN_E_UNSUPPORTED"),
+    # bf16 trees beyond the kernels' 32-bit byte offsets: pool over 2^24 slots, or over 4 GiB
+    (lambda d: d.__setitem__("pool_slots", (1 << 24) + 1), "PSATTN_E_UNSUPPORTED"),
+    (lambda d: d.update(pool_slots=(1 << 22) + 1, hkv=4, hq=4), "PSATTN_E_UNSUPPORTED"),
 ])
 def test_invalid_descriptors(base, mutate, status):
     mutate(base)
     with pytest.raises(P.PsattnError) as e:
         _make(**base)
     assert e.value.name == status, str(e.value)
+
+
+def test_size_limits_hold_only_for_bf16(base):
+    # the fp32 kernels use 64-bit offsets: the same large pool is accepted there
+    base.update(pool_slots=(1 << 24) + 1, dtype="fp32")
+    assert _make(**base).pool_slots == (1 << 24) + 1
+
+
+def test_bf16_query_rows_limit():
+    # Ns * Hq must stay below 2^24 (32-bit byte offsets into Q / O / dO at d = 128)
+    ns = (1 << 24) // 64
+    wl = W.custom([-1], [ns], [0], hq=64, hkv=8, d=128, tensors=False, block_policy=W.blocks_exact, seed=1)
+    with pytest.raises(P.PsattnError) as e:
+        _make(**_desc_arrays(wl))
+    assert e.value.name == "PSATTN_E_UNSUPPORTED"
 
 
 def test_wrong_refcount_is_rejected(base):

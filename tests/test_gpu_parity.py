@@ -105,10 +105,12 @@ def test_packed_siblings_with_split_prefix():
 # one-token root under a long child, many single-token roots
 DEGENERATE = {
     "one_token": dict(parent=[-1], seg=[1], samples=[0], hq=4, hkv=2, d=128, dtype="bf16"),
-    # (G = 1: the root key's dV sums 41 terms with P near 1/2; its error from the bf16 P of the dV
-    # product grows with the square root of that count, see the tolerance reading)
+    # the root key's dV and dK sum 41 x G terms with P near 1/2: a single bf16 rounding of P and dS
+    # drifts by ~0.0011 sqrt(n) (0.03 at G = 5, over the 2e-2 bound); the two-term split holds it
     "tiny_siblings": dict(parent=[-1] + [0] * 40, seg=[1] * 41, samples=list(range(1, 41)), hq=2, hkv=2, d=128,
                           dtype="bf16"),
+    "tiny_siblings_g5": dict(parent=[-1] + [0] * 40, seg=[1] * 41, samples=list(range(1, 41)), hq=5, hkv=1, d=128,
+                             dtype="bf16"),
     "token_chain": dict(parent=[-1] + list(range(69)), seg=[1] * 70, samples=[69, 30], hq=8, hkv=2, d=64,
                         dtype="bf16"),
     "short_root_long_child": dict(parent=[-1, 0], seg=[1, 700], samples=[1], hq=8, hkv=2, d=128, dtype="bf16"),
@@ -126,6 +128,20 @@ def test_degenerate_trees(name):
                   sigma=1.0 if c["dtype"] == "fp32" else 0.5, block_policy=W.blocks_exact)
     _say(f"degenerate {name} rows={wl.tree.num_rows}")
     H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+
+
+# attention-sink inputs: every query of a kv group puts about half its softmax weight on one root
+# key (scale q.k ~ log of the visible key count), so that key's dV and dK sum thousands of terms
+# with P near 1/2 (4096 (row, head) consumers here; a single bf16 rounding of P would leave
+# ~0.0011 sqrt(n P^2) ~ 0.04 of error on its dV)
+@pytest.mark.parametrize("sink_rows", [(0,), (0, 300)])
+def test_attention_sink(sink_rows):
+    wl = W.custom([-1] + [0] * 32, [512] + [16] * 32, list(range(1, 33)), hq=8, hkv=2, d=128, dtype="bf16", seed=21,
+                  block_policy=lambda L: W.blocks_fixed(L, 64))
+    W.add_attention_sink(wl, sink_rows, logit=float(np.log(528.0)))
+    _say(f"attention sink at rows {sink_rows}")
+    res = H.check_full(wl, H.run_gpu(wl), H.run_oracle(wl))
+    _say(f"sink {res}")
 
 
 # --------------------------------------------------------------------------- robustness and determinism
@@ -150,15 +166,42 @@ def test_pool_order_and_padding_do_not_change_results():
             assert np.array_equal(r1[i][w1.tree.row_slots()], r[i][w.tree.row_slots()])
 
 
-# --------------------------------------------------------------------------- full-size workloads (sampled)
+# --------------------------------------------------------------------------- full-size workloads
 
+# every kv head: all keys of the first and last 128-key tiles of the most-shared node and of a
+# leaf, O and LSE of every row consuming the most-shared node (every row, for c2 and c4), dQ of
+# the first and last query tiles of both nodes; the oracle evaluates them one by one
 @pytest.mark.parametrize("name", ["c2", "c2-small", "c3", "c4", "c5"])
-def test_full_size_sampled(name):
+def test_full_size(name):
     _say(f"{name}: generating")
     wl = W.make(name)
     _say(f"{name}: running GPU")
     gpu = H.run_gpu(wl)
-    _say(f"{name}: checking sampled outputs")
-    res = H.check_sampled(wl, gpu, kv_heads=(0, wl.hkv - 1))
-    _say(f"{name}: sampled {res}")
-    H.check_identities(wl, gpu)
+    _say(f"{name}: oracle on the selected outputs")
+    res = H.check_full_size(wl, gpu)
+    _say(f"{name}: full-size parity {res}")
+
+
+# the attention-sink input at the small-suffix probe's shape (4096-token prefix, 256 branches of
+# 16): root key 0 takes about half the softmax weight of each of its 8192 x 4 consumers per kv head
+def _sink_c2_small():
+    wl = W.make("c2-small")
+    W.add_attention_sink(wl, [0], logit=float(np.log(4112.0)))
+    return wl
+
+
+def test_full_size_attention_sink():
+    wl = _sink_c2_small()
+    _say("c2-small with an attention sink: running GPU")
+    gpu = H.run_gpu(wl)
+    res = H.check_full_size(wl, gpu, gate=("O", "LSE", "dK", "dV"))
+    _say(f"c2-small sink: full-size parity {res}")
+
+
+@pytest.mark.skip(reason="dQ takes Delta = dO . O from the bf16 O; on this input (rows whose softmax sits on one "
+                         "key) that leaves rel-L2 0.0067 > 5e-3 on the checked dQ rows (max-abs 0.0045); the "
+                         "correction pass for such rows is not built")
+def test_full_size_attention_sink_dq():
+    wl = _sink_c2_small()
+    res = H.check_full_size(wl, H.run_gpu(wl), gate=("dQ",))
+    _say(f"c2-small sink dQ: {res}")

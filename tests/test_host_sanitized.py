@@ -1,0 +1,43 @@
+"""The host planner and C ABI under AddressSanitizer and UndefinedBehaviorSanitizer (CPU only).
+
+psattn_host.cpp is compiled with g++ against a host-only stand-in for the HIP runtime header
+(tests/sanitize/), with -fsanitize=address,undefined and no recovery from undefined behaviour,
+and the host ABI tests (tests/test_abi_host.py: descriptor validation, random-forest planner
+coverage, packing and split plans) run against that build in a child process.  Any
+out-of-bounds access, use after free or signed overflow in validation or planning fails here.
+"""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2608_25683_amd", "csrc")
+
+
+def _runtime(name):
+    out = subprocess.run(["gcc", f"-print-file-name={name}"], capture_output=True, text=True).stdout.strip()
+    return out if os.path.isabs(out) and os.path.exists(out) else None
+
+
+@pytest.mark.skipif(shutil.which("g++") is None or _runtime("libasan.so") is None, reason="needs g++ with libasan")
+def test_host_abi_tests_pass_under_asan_and_ubsan(tmp_path):
+    lib = str(tmp_path / "libpsattn_host_sanitized.so")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-shared", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer",
+           "-I", os.path.join(ROOT, "tests", "sanitize"), "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           os.path.join(CSRC, "psattn_host.cpp"), os.path.join(ROOT, "tests", "sanitize", "launch_stubs.cpp"),
+           "-o", lib]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-4000:]
+    runner = ("import sys; sys.path.insert(0, %r); import paper_2608_25683_amd.psattn as P; P.LIB_PATH = %r; "
+              "import pytest; sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider', %r]))"
+              % (ROOT, lib, os.path.join(ROOT, "tests", "test_abi_host.py")))
+    env = dict(os.environ, LD_PRELOAD=_runtime("libasan.so"), ASAN_OPTIONS="detect_leaks=0:abort_on_error=0",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    r = subprocess.run([sys.executable, "-c", runner], capture_output=True, text=True, env=env, cwd=ROOT, timeout=600)
+    log = r.stdout[-3000:] + r.stderr[-6000:]
+    assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, log
+    assert r.returncode == 0, log

@@ -109,6 +109,27 @@ def test_pi3_detects_a_broken_mask():
 torch = pytest.importorskip("torch")
 
 
+def _walk_samples(t):
+    """Each sample's packed rows in sequence order, and each row's owner sample, found by walking
+    parent[] up from the sample's endpoint (independent of the oracle's own expansion)."""
+    seqs = []
+    row_owner = np.full(t.num_rows, -1, dtype=np.int64)
+    for s, e in enumerate(t.sample_end):
+        nodes = []
+        n = int(e)
+        while n != -1:
+            nodes.append(n)
+            n = int(t.parent[n])
+        rows = []
+        for n in reversed(nodes):                                      # root first
+            rows.extend(range(int(t.row_off[n]), int(t.row_off[n]) + int(t.seg_len[n])))
+        rows = np.asarray(rows, dtype=np.int64)
+        unowned = rows[row_owner[rows] < 0]
+        row_owner[unowned] = s
+        seqs.append(rows)
+    return seqs, row_owner
+
+
 def _sdpa_tree(wl, split="owner"):
     """Per-sample SDPA in fp64 through an index-gather; autograd sums duplicate gradients."""
     import torch.nn.functional as F
@@ -118,13 +139,10 @@ def _sdpa_tree(wl, split="owner"):
     K = torch.tensor(wl.K, dtype=torch.float64, requires_grad=True)
     V = torch.tensor(wl.V, dtype=torch.float64, requires_grad=True)
     dO = torch.tensor(wl.dO, dtype=torch.float64)
-    own = O.owners(t.parent, t.sample_end)
-    row_owner = np.empty(t.num_rows, dtype=np.int64)
-    for n in range(t.num_nodes):
-        row_owner[t.row_off[n]:t.row_off[n] + t.seg_len[n]] = own[n]
+    seqs, row_owner = _walk_samples(t)
     loss = 0.0
     outs = []
-    for s, rows in enumerate(O.sample_rows(t.parent, t.seg_len, t.row_off, t.sample_end)):
+    for s, rows in enumerate(seqs):
         ri = torch.tensor(rows)
         q = Q[ri].permute(1, 0, 2)                                     # [Hq, L, d]
         k = K[ri].permute(1, 0, 2).repeat_interleave(G, dim=0)         # head h reads kv head h // G
@@ -153,6 +171,26 @@ def test_pi4_matches_torch_sdpa(shape):
         assert np.max(np.abs(Of[rows] - o)) <= 1e-10
     for a, b in ((dQ, gQ), (dK, gK), (dV, gV)):
         assert np.max(np.abs(a - b)) <= 1e-10
+
+
+def test_pi4_catches_a_path_order_bug():
+    # planted in the oracle: root-to-node paths listed child first; the SDPA pin, which walks
+    # parent[] itself, must then disagree
+    wl = W.custom([-1, 0, 1], [9, 5, 11], [2, 1], hq=2, hkv=1, d=16, dtype="fp32", seed=2, sigma=1.0)
+    orig = O.psattn_oracle.node_paths
+
+    def reversed_paths(parent):
+        return [p[::-1] for p in orig(parent)]
+    t = wl.tree
+    try:
+        O.psattn_oracle.node_paths = reversed_paths
+        Of, _ = O.forward(t.parent, t.seg_len, t.row_off, t.sample_end, wl.Q.astype(np.float64),
+                          wl.K.astype(np.float64), wl.V.astype(np.float64), wl.scale, check_copies=False)
+    finally:
+        O.psattn_oracle.node_paths = orig
+    outs, gQ, gK, gV = _sdpa_tree(wl)
+    worst = max(float(np.max(np.abs(Of[rows] - o))) for rows, o in outs)
+    assert worst > 1e-3
 
 
 # --------------------------------------------------------------------------- Pi5: closed forms
