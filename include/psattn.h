@@ -156,6 +156,20 @@ psattn_status psattn_bwd(const psattn_tree* tree, const void* Q, const void* K, 
                          const void* O, const float* LSE, const void* dO,
                          float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): psattn_bwd with its workspace taken from a file-scope
+ * device array of PSATTN_NOALLOC_SCRATCH_MIB MiB, one copy per GPU, held until the process ends.
+ * It calls no hipMalloc/hipFree and allocates nothing else.  Arguments and results as for
+ * psattn_bwd, without ws / ws_bytes.  A tree whose backward workspace (psattn_workspace_size,
+ * pass 1) exceeds the array is rejected with PSATTN_E_WORKSPACE before anything is enqueued.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU (other streams,
+ * other host threads) race and must be serialised by the caller.  The array needs no clearing:
+ * each call writes every workspace byte it reads. */
+#define PSATTN_NOALLOC_SCRATCH_MIB 128
+psattn_status psattn_bwd_noalloc(const psattn_tree* tree, const void* Q, const void* K, const void* V,
+                                 const void* O, const float* LSE, const void* dO,
+                                 float* dQ, float* dK, float* dV, void* stream);
+
 /* Reference count of every node: the number of samples whose path holds it
  * (Sec. 5.2).  node_refcount has num_nodes entries. */
 psattn_status psattn_tree_refcounts(const psattn_tree* tree, int32_t* node_refcount);

@@ -38,6 +38,11 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 }  // namespace
 
+namespace psattn {
+// the thread-local last-error message, for the library's other sources
+psattn_status set_error(psattn_status st, const char* msg) { return fail(st, "%s", msg); }
+}  // namespace psattn
+
 struct psattn_tree {
   // descriptor (copied)
   int32_t N = 0, S = 0, hq = 0, hkv = 0, d = 0;

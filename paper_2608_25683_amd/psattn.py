@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpsattn.s
 
 PSATTN_BF16 = 0
 PSATTN_FP32 = 1
+NOALLOC_SCRATCH_MIB = 128   # PSATTN_NOALLOC_SCRATCH_MIB: workspace limit of psattn_bwd_noalloc
 
 STATUS = {
     0: "PSATTN_OK", -1: "PSATTN_E_INVALID_ARG", -2: "PSATTN_E_INVALID_TREE", -3: "PSATTN_E_BLOCK_RANGE",
@@ -31,7 +32,8 @@ STATUS = {
 
 EXPORTED = [
     "psattn_tree_create", "psattn_tree_destroy", "psattn_tree_device_bytes", "psattn_tree_upload",
-    "psattn_workspace_size", "psattn_fwd", "psattn_bwd", "psattn_tree_refcounts", "psattn_tree_get_info",
+    "psattn_workspace_size", "psattn_fwd", "psattn_bwd", "psattn_bwd_noalloc", "psattn_tree_refcounts",
+    "psattn_tree_get_info",
     "psattn_tree_plan_array", "psattn_profile_enable", "psattn_profile_reset", "psattn_profile_read",
     "psattn_status_string", "psattn_last_error",
 ]
@@ -99,6 +101,7 @@ def lib() -> ctypes.CDLL:
         L.psattn_workspace_size.argtypes = [vp, ctypes.c_int, ctypes.POINTER(sz)]
         L.psattn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.psattn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.psattn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.psattn_tree_refcounts.argtypes = [vp, _i32p]
         L.psattn_tree_get_info.argtypes = [vp, ctypes.POINTER(TreeInfo)]
         L.psattn_tree_plan_array.argtypes = [vp, ctypes.c_int, ctypes.POINTER(_i32p), _i64p, _i32p]
@@ -310,6 +313,25 @@ def psattn_bwd(tree: Tree, Q, K, V, O, LSE, dO, dQ=None, dK=None, dV=None, ws=No
     stream = torch.cuda.current_stream(Q.device).cuda_stream
     _check(lib().psattn_bwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(dO), _vp(dQ), _vp(dK),
                             _vp(dV), _vp(ws), ws.numel(), ctypes.c_void_p(stream)))
+    return dQ, dK, dV
+
+
+def psattn_bwd_noalloc(tree: Tree, Q, K, V, O, LSE, dO, dQ, dK, dV):
+    """psattn_bwd with its workspace in the library's per-GPU device array (no workspace argument,
+    nothing allocated by the library); the output tensors are the caller's."""
+    import torch
+    if tree._plan_buf is None:
+        raise RuntimeError("tree not uploaded (call Tree.upload)")
+    dt = _torch_dtype(tree)
+    ns, hq, hkv, d, ps = tree.num_rows, tree.hq, tree.hkv, tree.head_dim, tree.pool_slots
+    f32 = torch.float32
+    for x, shape, t, name in ((Q, (ns, hq, d), dt, "Q"), (K, (ps, hkv, d), dt, "K"), (V, (ps, hkv, d), dt, "V"),
+                              (O, (ns, hq, d), dt, "O"), (LSE, (hq, ns), f32, "LSE"), (dO, (ns, hq, d), dt, "dO"),
+                              (dQ, (ns, hq, d), f32, "dQ"), (dK, (ps, hkv, d), f32, "dK"), (dV, (ps, hkv, d), f32, "dV")):
+        _need(x, shape, t, name)
+    stream = torch.cuda.current_stream(Q.device).cuda_stream
+    _check(lib().psattn_bwd_noalloc(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(dO), _vp(dQ), _vp(dK),
+                                    _vp(dV), ctypes.c_void_p(stream)))
     return dQ, dK, dV
 
 

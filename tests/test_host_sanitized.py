@@ -1,6 +1,7 @@
 """The host planner and C ABI under AddressSanitizer and UndefinedBehaviorSanitizer (CPU only).
 
-psattn_host.cpp is compiled with g++ against a host-only stand-in for the HIP runtime header
+psattn_host.cpp and the host side of psattn_noalloc.hip are compiled with g++ against a host-only
+stand-in for the HIP runtime header
 (tests/sanitize/), with -fsanitize=address,undefined and no recovery from undefined behaviour,
 and the host ABI tests (tests/test_abi_host.py: descriptor validation, random-forest planner
 coverage, packing and split plans) run against that build in a child process.  Any
@@ -29,6 +30,7 @@ def test_host_abi_tests_pass_under_asan_and_ubsan(tmp_path):
            "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer",
            "-I", os.path.join(ROOT, "tests", "sanitize"), "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(CSRC, "psattn_host.cpp"), os.path.join(ROOT, "tests", "sanitize", "launch_stubs.cpp"),
+           "-x", "c++", os.path.join(CSRC, "psattn_noalloc.hip"), "-x", "none",
            "-o", lib]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-4000:]
