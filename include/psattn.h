@@ -17,12 +17,17 @@
  *   consumer of a shared token and runs once (Sec. 6, training runtime).
  *
  * Layouts (row-major, all device pointers 16-byte aligned):
- *   Q, O, dO        [Ns][Hq][d]      Ns = sum of segment lengths, rows of node
+ *   Q, O, dO        [Ns][Hq][d]      Ns = sum of internal segment lengths, rows of node
  *                                    i at row_off[i] .. row_off[i]+seg_len[i]-1
  *   dQ              [Ns][Hq][d]      fp32
  *   K, V            [pool_slots][Hkv][d]   token t of a block at slot base+t
- *   dK, dV          [pool_slots][Hkv][d]   fp32; slots holding no token are
- *                                    written 0
+ *   dK, dV          [pool_slots][Hkv][d]   fp32; written for the tokens of
+ *                                    internal nodes, added to for the tokens of
+ *                                    external nodes (the accumulators of cached
+ *                                    blocks, complete once the block's last
+ *                                    consuming call has run: Sec. 5.2), zero on
+ *                                    the unused slots of internal nodes' blocks;
+ *                                    every other slot is left untouched
  *   LSE             [Hq][Ns]         fp32, natural log of the softmax
  *                                    denominator (scale included)
  *   dtype PSATTN_BF16: Q/K/V/O/dO bf16; LSE/dQ/dK/dV fp32.
@@ -86,7 +91,13 @@ typedef struct {
   int32_t num_nodes;
   const int32_t* parent;      /* [num_nodes]; parent[i] < i, or -1 for a root (forests allowed) */
   const int32_t* seg_len;     /* [num_nodes]; >= 1 */
-  const int64_t* row_off;     /* [num_nodes]; the row ranges must tile [0, Ns) exactly */
+  const int64_t* row_off;     /* [num_nodes]; the row ranges of the internal nodes must tile
+                                 [0, Ns) exactly.  row_off[i] = -1 marks an external node:
+                                 one an earlier call computed (Sec. 4.1.1 inter-batch sharing,
+                                 Sec. 4.1.2 self-sequence sharing).  Its K/V are read from its
+                                 blocks, it has no query rows here, its parent (if any) must be
+                                 external too, no sample may end at it, and the backward adds
+                                 this call's share of its dK/dV to what dK/dV already hold. */
   const int32_t* blk_ptr;     /* [num_nodes+1]; node i owns blocks[blk_ptr[i] .. blk_ptr[i+1]) */
   const psattn_block* blocks;
   int64_t pool_slots;         /* slots in the K/V pool (< 2^31) */

@@ -550,10 +550,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       kdst = a.part_dk + o;
       vdst = a.part_dv + o;
     }
+    if (it.part < 0 && it.acc) {   // a cached node's keys: add to the gradients of earlier calls
 #pragma unroll
-    for (int nb = 0; nb < DB; ++nb) {
-      kdst[32 * nb + l32] = dk[nb][v] * scale;
-      vdst[32 * nb + l32] = dv[nb][v];
+      for (int nb = 0; nb < DB; ++nb) {
+        kdst[32 * nb + l32] += dk[nb][v] * scale;
+        vdst[32 * nb + l32] += dv[nb][v];
+      }
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < DB; ++nb) {
+        kdst[32 * nb + l32] = dk[nb][v] * scale;
+        vdst[32 * nb + l32] = dv[nb][v];
+      }
     }
   }
 }
@@ -1030,10 +1038,11 @@ __global__ __launch_bounds__(256) void bwd_kv_f32_kernel(BwdArgs a) {
     kd = a.part_dk + o;
     vd = a.part_dv + o;
   }
+  const bool acc = it.part < 0 && it.acc;   // a cached node's keys: add to earlier calls' gradients
 #pragma unroll
   for (int i = 0; i < H; ++i) {
-    kd[i] = dk[i] * a.s.scale;
-    vd[i] = dv[i];
+    kd[i] = dk[i] * a.s.scale + (acc ? kd[i] : 0.f);
+    vd[i] = dv[i] + (acc ? vd[i] : 0.f);
   }
 }
 
@@ -1171,7 +1180,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   }
 }
 
-// dK/dV = sum of partial tiles in ascending chunk order
+// dK/dV = sum of partial tiles in ascending chunk order (added to dK/dV for a cached node's keys)
 __global__ __launch_bounds__(256) void bwd_reduce_kv_kernel(BwdArgs a) {
   const ReduceEntry e = a.plan.reduce[blockIdx.x];
   const int D = a.s.d;
@@ -1185,6 +1194,10 @@ __global__ __launch_bounds__(256) void bwd_reduce_kv_kernel(BwdArgs a) {
       sv += *(const f32x4*)(a.part_dv + o);
     }
     const size_t o = (size_t)a.plan.kv_list[e.kv_off + k] * kv_stride + (size_t)e.hk * D + d4;
+    if (e.acc) {
+      sk = *(const f32x4*)(a.dK + o) + sk;
+      sv = *(const f32x4*)(a.dV + o) + sv;
+    }
     *(f32x4*)(a.dK + o) = sk;
     *(f32x4*)(a.dV + o) = sv;
   }

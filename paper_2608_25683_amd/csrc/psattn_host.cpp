@@ -54,6 +54,7 @@ struct psattn_tree {
   std::vector<psattn_block> blocks;
   // derived tree facts
   std::vector<int64_t> off;        // sequence position of each node's first token
+  std::vector<char> ext;           // node cached by an earlier call: K/V in the pool, no query rows here
   std::vector<int32_t> refcount;   // samples whose path holds the node (Sec. 5.2)
   std::vector<std::vector<int32_t>> children;
   int64_t Ns = 0, Nu = 0, nvis = 0;
@@ -110,8 +111,10 @@ psattn_status validate_and_copy(const psattn_tree_desc* d, psattn_tree* t) {
   t->blk_ptr.assign(d->blk_ptr, d->blk_ptr + N + 1);
   t->sample_end.assign(d->sample_end, d->sample_end + t->S);
 
-  // parents precede children; segments non-empty
+  // parents precede children; segments non-empty; external (cached) nodes only above external
+  // nodes, so that they form a prefix of every path that holds them (Sec. 4.1.1, 4.1.2)
   t->off.assign(N, 0);
+  t->ext.assign(N, 0);
   t->children.assign(N, {});
   int64_t ns = 0;
   for (int i = 0; i < N; ++i) {
@@ -119,11 +122,15 @@ psattn_status validate_and_copy(const psattn_tree_desc* d, psattn_tree* t) {
     if (p < -1 || p >= i)
       return fail(PSATTN_E_INVALID_TREE, "parent[%d] = %d: a parent must precede its child (or be -1)", i, p);
     if (t->seg_len[i] < 1) return fail(PSATTN_E_INVALID_TREE, "seg_len[%d] = %d: segments must be non-empty", i, t->seg_len[i]);
+    t->ext[i] = t->row_off[i] < 0;
+    if (t->ext[i] && p >= 0 && !t->ext[p])
+      return fail(PSATTN_E_INVALID_TREE, "node %d is external (row_off < 0) but its parent %d is not", i, p);
     t->off[i] = p < 0 ? 0 : t->off[p] + t->seg_len[p];
     if (p >= 0) t->children[p].push_back(i);
-    ns += t->seg_len[i];
+    if (!t->ext[i]) ns += t->seg_len[i];
     if (t->off[i] + t->seg_len[i] > INT32_MAX) return fail(PSATTN_E_UNSUPPORTED, "sequence of node %d too long", i);
   }
+  if (ns < 1) return fail(PSATTN_E_INVALID_TREE, "every node is external: the call has no query rows");
   if (ns > INT32_MAX / 2) return fail(PSATTN_E_UNSUPPORTED, "too many rows (%lld)", (long long)ns);
   t->Ns = ns;
   if (t->dtype == PSATTN_BF16) {
@@ -138,13 +145,14 @@ psattn_status validate_and_copy(const psattn_tree_desc* d, psattn_tree* t) {
                   (long long)ns, t->hq);
   }
 
-  // row ranges tile [0, Ns)
+  // row ranges of the internal nodes tile [0, Ns)
   {
-    std::vector<int> ord(N);
-    std::iota(ord.begin(), ord.end(), 0);
+    std::vector<int> ord;
+    for (int i = 0; i < N; ++i)
+      if (!t->ext[i]) ord.push_back(i);
     std::sort(ord.begin(), ord.end(), [&](int a, int b) { return t->row_off[a] < t->row_off[b]; });
     int64_t cur = 0;
-    for (int k = 0; k < N; ++k) {
+    for (size_t k = 0; k < ord.size(); ++k) {
       int i = ord[k];
       if (t->row_off[i] != cur)
         return fail(PSATTN_E_INVALID_TREE, "row_off[%d] = %lld: node row ranges must tile [0, Ns) without gaps or overlap",
@@ -197,8 +205,11 @@ psattn_status validate_and_copy(const psattn_tree_desc* d, psattn_tree* t) {
   for (int s = 0; s < t->S; ++s) {
     int e = t->sample_end[s];
     if (e < 0 || e >= N) return fail(PSATTN_E_INVALID_TREE, "sample_end[%d] = %d out of range", s, e);
-    nu += t->off[e] + t->seg_len[e];
-    for (int n = e; n >= 0; n = t->parent[n]) t->refcount[n]++;
+    if (t->ext[e]) return fail(PSATTN_E_INVALID_TREE, "sample_end[%d] = %d is an external node (no query rows here)", s, e);
+    for (int n = e; n >= 0; n = t->parent[n]) {
+      t->refcount[n]++;
+      if (!t->ext[n]) nu += t->seg_len[n];   // unshared-equivalent query tokens of this call
+    }
   }
   t->Nu = nu;
   for (int i = 0; i < N; ++i) {
@@ -211,6 +222,7 @@ psattn_status validate_and_copy(const psattn_tree_desc* d, psattn_tree* t) {
   }
   int64_t nvis = 0;
   for (int i = 0; i < N; ++i) {
+    if (t->ext[i]) continue;
     int64_t L = t->seg_len[i];
     nvis += L * t->off[i] + L * (L + 1) / 2;
   }
@@ -255,14 +267,14 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   const int n_chunks = t->hq / s.hc;  // head chunks per forward task
   const int num_cus = o.num_cus > 0 ? o.num_cus : 256;
 
-  // slot of every packed row, and sequence position of every row
-  std::vector<int32_t> slot_of_row(t->Ns);
+  // pool slots of every node's tokens, and sequence position of every packed row
+  std::vector<std::vector<int32_t>> node_slots(N);
   t->row_pos.assign(t->Ns, 0);
   for (int n = 0; n < N; ++n) {
-    int64_t r = t->row_off[n];
     for (int b = t->blk_ptr[n]; b < t->blk_ptr[n + 1]; ++b)
-      for (int k = 0; k < t->blocks[b].len; ++k) slot_of_row[r++] = (int32_t)(t->blocks[b].base + k);
-    for (int a = 0; a < t->seg_len[n]; ++a) t->row_pos[t->row_off[n] + a] = (int32_t)(t->off[n] + a);
+      for (int k = 0; k < t->blocks[b].len; ++k) node_slots[n].push_back((int32_t)(t->blocks[b].base + k));
+    if (!t->ext[n])
+      for (int a = 0; a < t->seg_len[n]; ++a) t->row_pos[t->row_off[n] + a] = (int32_t)(t->off[n] + a);
   }
 
   // per-node path slot list: slots of sequence positions 0 .. off+len-1
@@ -273,8 +285,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     for (int m = n; m >= 0; m = t->parent[m]) path.push_back(m);
     std::reverse(path.begin(), path.end());
     kvoff[n] = (int64_t)t->kv_list.size();
-    for (int m : path)
-      for (int a = 0; a < t->seg_len[m]; ++a) t->kv_list.push_back(slot_of_row[t->row_off[m] + a]);
+    for (int m : path) t->kv_list.insert(t->kv_list.end(), node_slots[m].begin(), node_slots[m].end());
     if (t->kv_list.size() > (size_t)INT32_MAX) return fail(PSATTN_E_UNSUPPORTED, "key lists exceed 2^31 entries");
   }
 
@@ -285,7 +296,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   t->q_list.clear();
   int64_t total_f = 0;
   for (int n = 0; n < N; ++n)
-    for (int a0 = 0; a0 < t->seg_len[n]; a0 += s.bmq) {
+    for (int a0 = 0; !t->ext[n] && a0 < t->seg_len[n]; a0 += s.bmq) {
       int a1 = std::min<int>(t->seg_len[n], a0 + s.bmq);
       total_f += (int64_t)(a1 - a0) * (t->off[n] + a1);
     }
@@ -320,7 +331,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       rows = 0;
     };
     for (int c : t->children[p]) {
-      if (2 * t->seg_len[c] > s.bmq) continue;
+      if (t->ext[c] || 2 * t->seg_len[c] > s.bmq) continue;
       if (rows + t->seg_len[c] > s.bmq) flush();
       cur.push_back(c);
       rows += t->seg_len[c];
@@ -372,7 +383,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     }
   }
   for (int n = 0; n < N; ++n) {
-    if (packed[n]) continue;
+    if (packed[n] || t->ext[n]) continue;
     for (int a0 = 0; a0 < t->seg_len[n]; a0 += s.bmq) {
       int a1 = std::min<int>(t->seg_len[n], a0 + s.bmq);
       int nq = a1 - a0;
@@ -422,8 +433,9 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   }
 
   // ---------------- dK/dV tasks: key tile x consumer-row chunk ----------------
-  // consumer list of node m: every row of every descendant (node order), then m's own rows from
-  // its last position down to 0; the tile starting at key b0 uses the list up to own position b0
+  // consumer list of node m: every row of every (internal) descendant (node order), then m's own
+  // rows from its last position down to 0; the tile starting at key b0 uses the list up to own
+  // position b0.  An external node has no own rows: all its consumers see every key of a tile.
   std::vector<int64_t> cons_off(N), cons_len(N), desc_len(N);
   for (int m = 0; m < N; ++m) {
     cons_off[m] = (int64_t)t->q_list.size();
@@ -437,9 +449,9 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     }
     std::sort(sub.begin(), sub.end());
     for (int x : sub)
-      for (int a = 0; a < t->seg_len[x]; ++a) t->q_list.push_back((int32_t)(t->row_off[x] + a));
+      for (int a = 0; !t->ext[x] && a < t->seg_len[x]; ++a) t->q_list.push_back((int32_t)(t->row_off[x] + a));
     desc_len[m] = (int64_t)t->q_list.size() - cons_off[m];
-    for (int a = t->seg_len[m] - 1; a >= 0; --a) t->q_list.push_back((int32_t)(t->row_off[m] + a));
+    for (int a = t->seg_len[m] - 1; !t->ext[m] && a >= 0; --a) t->q_list.push_back((int32_t)(t->row_off[m] + a));
     cons_len[m] = (int64_t)t->q_list.size() - cons_off[m];
     if (t->q_list.size() > (size_t)INT32_MAX) return fail(PSATTN_E_UNSUPPORTED, "row lists exceed 2^31 entries");
   }
@@ -447,7 +459,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   for (int m = 0; m < N; ++m)
     for (int b0 = 0; b0 < t->seg_len[m]; b0 += BKV_TILE) {
       int nk = std::min(BKV_TILE, t->seg_len[m] - b0);
-      total_b += (int64_t)nk * (cons_len[m] - b0);
+      total_b += (int64_t)nk * (cons_len[m] - (t->ext[m] ? 0 : b0));
     }
   int64_t chunk_rows;
   if (o.bwd_q_chunk > 0) {
@@ -458,16 +470,19 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     int64_t per_cu = total_b * t->hkv / std::max(1, 2 * num_cus);
     chunk_rows = std::max<int64_t>(2048, per_cu / BKV_TILE / Q_SUB * Q_SUB);
   }
-  struct BTask { int32_t kv_off, nk, kv_pos0, q_off, nq, mask_lo, mask_hi, part_base, nparts, chunk; double cost; };
+  struct BTask { int32_t kv_off, nk, kv_pos0, q_off, nq, mask_lo, mask_hi, part_base, nparts, chunk, acc; double cost; };
   std::vector<BTask> btasks;
   std::vector<ReduceEntry> reduces;
   int64_t part_tiles = 0;
   for (int m = 0; m < N; ++m) {
     for (int b0 = 0; b0 < t->seg_len[m]; b0 += BKV_TILE) {
       int nk = std::min(BKV_TILE, t->seg_len[m] - b0);
-      int64_t nq_total = cons_len[m] - b0;
+      // an external node's tiles add this call's consumers to the gradients that earlier calls
+      // left in dK/dV (the cached block's accumulators)
+      const int acc = t->ext[m] ? 1 : 0;
+      int64_t nq_total = cons_len[m] - (acc ? 0 : b0);
       // own rows at positions b0 .. b0+nk-2 see only part of the tile: the last nk-1 list entries
-      const int64_t mlo = nq_total - (nk - 1), mhi = nq_total;
+      const int64_t mlo = acc ? nq_total : nq_total - (nk - 1), mhi = nq_total;
       int nparts = chunk_rows == INT64_MAX ? 1 : (int)((nq_total + chunk_rows - 1) / chunk_rows);
       int32_t kv_off = (int32_t)(kvoff[m] + t->off[m] + b0);
       int32_t kv_pos0 = (int32_t)(t->off[m] + b0);
@@ -475,7 +490,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       if (nparts > 1) {
         part_base = (int32_t)part_tiles;
         part_tiles += (int64_t)nparts * t->hkv;
-        for (int hk = 0; hk < t->hkv; ++hk) reduces.push_back({kv_off, nk, hk, part_base + hk * nparts, nparts, {0, 0, 0}});
+        for (int hk = 0; hk < t->hkv; ++hk) reduces.push_back({kv_off, nk, hk, part_base + hk * nparts, nparts, acc, {0, 0}});
       }
       for (int j = 0; j < nparts; ++j) {
         int64_t c0 = nparts > 1 ? j * chunk_rows : 0;
@@ -491,6 +506,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
         b.part_base = part_base;
         b.nparts = nparts;
         b.chunk = j;
+        b.acc = acc;
         b.cost = (double)b.nq * nk + 4096.0;
         btasks.push_back(b);
       }
@@ -507,19 +523,19 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       const BTask& b = btasks[i];
       for (int hk = 0; hk < t->hkv; ++hk) {
         int32_t part = b.nparts > 1 ? b.part_base + hk * b.nparts + b.chunk : -1;
-        t->bkv.push_back({b.kv_off, b.nk, b.kv_pos0, b.q_off, b.nq, hk, part, b.mask_lo, b.mask_hi, 0});
+        t->bkv.push_back({b.kv_off, b.nk, b.kv_pos0, b.q_off, b.nq, hk, part, b.mask_lo, b.mask_hi, b.acc});
       }
     }
   }
 
-  // ---------------- pool slots that hold no token ----------------
-  {
-    std::vector<uint8_t> used(t->pool_slots, 0);
-    for (const psattn_block& B : t->blocks)
-      for (int k = 0; k < B.len; ++k) used[B.base + k] = 1;
-    t->pad_slots.clear();
-    for (int64_t x = 0; x < t->pool_slots; ++x)
-      if (!used[x]) t->pad_slots.push_back((int32_t)x);
+  // ---------------- slots of this call's blocks that hold no token ----------------
+  // (the padding of internal nodes' blocks; the rest of the pool -- other trees, cached blocks --
+  // is left untouched)
+  t->pad_slots.clear();
+  for (int n = 0; n < N; ++n) {
+    if (t->ext[n]) continue;
+    for (int b = t->blk_ptr[n]; b < t->blk_ptr[n + 1]; ++b)
+      for (int k = t->blocks[b].len; k < t->blocks[b].capacity; ++k) t->pad_slots.push_back((int32_t)(t->blocks[b].base + k));
   }
 
   if (t->fwd.size() > (size_t)INT32_MAX || t->bkv.size() > (size_t)INT32_MAX)

@@ -49,14 +49,15 @@ struct BkvItem {
   int32_t part;      // -1: write dK/dV directly; else partial tile index
   int32_t mask_lo;   // chunk rows [mask_lo, mask_hi) may see only part of the keys;
   int32_t mask_hi;   //   every other row sees all of them
-  int32_t pad_;
+  int32_t acc;       // 1: a cached (external) node's keys: add to dK/dV instead of writing them
 };
 
 struct ReduceEntry {  // a key tile whose consumer rows were split into chunks
   int32_t kv_off, nk, hk;
   int32_t part0;      // chunk j wrote partial tile part0 + j
   int32_t nparts;
-  int32_t pad[3];
+  int32_t acc;        // 1: add the sum to dK/dV (a cached node's keys)
+  int32_t pad[2];
 };
 
 // Device-side view of an uploaded plan.

@@ -70,7 +70,8 @@ class Tree:
 
     @property
     def num_rows(self) -> int:
-        return int(self.seg_len.sum())
+        """Query rows of this call: nodes with row_off < 0 are external (cached by an earlier call)."""
+        return int(self.seg_len[self.row_off >= 0].sum())
 
     def node_offsets(self) -> np.ndarray:
         """Sum of ancestor segment lengths per node (the sequence position of its first token)."""
@@ -91,6 +92,8 @@ class Tree:
         """Pool slot holding each packed row's K/V (int64 [Ns])."""
         slots = np.empty(self.num_rows, dtype=np.int64)
         for n in range(self.num_nodes):
+            if self.row_off[n] < 0:
+                continue
             t = int(self.row_off[n])
             for b in range(int(self.blk_ptr[n]), int(self.blk_ptr[n + 1])):
                 ln = int(self.blk_len[b])
@@ -439,6 +442,57 @@ def add_attention_sink(wl: Workload, key_rows: Sequence[int], logit: float) -> W
             Q[:, h] += (logit / wl.scale) * k / float(k @ k)
     wl.Q = _round(Q, wl.dtype)
     return wl
+
+
+def call_subset(wl: Workload, ends: Sequence[int], external: Sequence[int] = ()) -> Tuple[Workload, np.ndarray]:
+    """One call of a forest processed over several calls (micro-batches that reuse a cached prefix,
+    Sec. 4.1.1 inter-batch sharing and 4.1.2 self-sequence sharing).
+
+    The call's samples end at the forest nodes ``ends`` (a chunk of a long sequence ends at the
+    chunk's node); it holds the nodes on their paths, in the forest's node order.  Forest nodes in ``external`` are cached by an earlier call: their K/V stay in the
+    shared pool, they get no query rows (row_off = -1), and the backward adds this call's share of
+    their dK/dV to what the earlier calls left.  Returns the call's workload (same pool, K/V and
+    page blocks; Q and dO of its own rows; sample ends remapped) and, for each of its rows, the
+    forest row it is.  The adjoint dO of a row is the forest's total adjoint of that token.
+    """
+    t = wl.tree
+    ext = set(int(x) for x in external)
+    keep = set()
+    for e in ends:
+        n = int(e)
+        while n >= 0:
+            keep.add(n)
+            n = int(t.parent[n])
+    nodes = sorted(keep)
+    new_of = {n: i for i, n in enumerate(nodes)}
+    parent = np.array([new_of[int(t.parent[n])] if t.parent[n] >= 0 else -1 for n in nodes], dtype=np.int32)
+    seg = t.seg_len[nodes].astype(np.int32)
+    row_off = np.full(len(nodes), -1, dtype=np.int64)
+    rows = []
+    cur = 0
+    for i, n in enumerate(nodes):
+        if n in ext:
+            continue
+        row_off[i] = cur
+        rows.extend(range(int(t.row_off[n]), int(t.row_off[n]) + int(t.seg_len[n])))
+        cur += int(t.seg_len[n])
+    blk_ptr = [0]
+    bidx = []
+    for n in nodes:
+        bidx.extend(range(int(t.blk_ptr[n]), int(t.blk_ptr[n + 1])))
+        blk_ptr.append(len(bidx))
+    bidx = np.asarray(bidx, dtype=np.int64)
+    tree = Tree(parent=parent, seg_len=seg, row_off=row_off, blk_ptr=np.asarray(blk_ptr, dtype=np.int32),
+                blk_base=t.blk_base[bidx], blk_cap=t.blk_cap[bidx], blk_len=t.blk_len[bidx], blk_pos=t.blk_pos[bidx],
+                pool_slots=t.pool_slots,
+                sample_end=np.array([new_of[int(e)] for e in ends], dtype=np.int32))
+    rows = np.asarray(rows, dtype=np.int64)
+    sub = Workload(name=f"{wl.name}-call", tree=tree, hq=wl.hq, hkv=wl.hkv, d=wl.d, dtype=wl.dtype, scale=wl.scale)
+    if wl.Q is not None:
+        sub.Q, sub.dO = wl.Q[rows], wl.dO[rows]
+        sub.K, sub.V = wl.K[rows], wl.V[rows]
+        sub.K_pool, sub.V_pool = wl.K_pool, wl.V_pool
+    return sub, rows
 
 
 def scatter_pool(tree: Tree, K: np.ndarray, V: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:

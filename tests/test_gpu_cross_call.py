@@ -1,0 +1,101 @@
+"""Cross-call prefix reuse on the GPU (Sec. 4.1.1 inter-batch sharing, Sec. 4.1.2 self-sequence
+sharing, Sec. 5.2 reference counts): a forest processed over several calls, each later call
+reading the cached K/V of nodes an earlier call computed and adding its share of their dK/dV to
+the same fp32 accumulators.  After the last call the outputs of every call and the accumulated
+dK/dV match the fp64 oracle on the whole forest, at the bf16 tolerances.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2608_25683_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+import parity_helpers as H  # noqa: E402
+
+
+def _run_calls(forest, calls, opts=None):
+    """Run the calls in order on one pool with shared dK/dV; return forest-shaped outputs."""
+    from paper_2608_25683_amd import psattn as P
+    dev = torch.device("cuda")
+    t = forest.tree
+    K = torch.from_numpy(forest.K_pool).to(dev).to(torch.bfloat16)
+    V = torch.from_numpy(forest.V_pool).to(dev).to(torch.bfloat16)
+    dK = torch.full((t.pool_slots, forest.hkv, forest.d), float("nan"), dtype=torch.float32, device=dev)
+    dV = torch.full_like(dK, float("nan"))
+    Of = np.zeros((t.num_rows, forest.hq, forest.d))
+    LSEf = np.zeros((forest.hq, t.num_rows))
+    dQf = np.zeros((t.num_rows, forest.hq, forest.d))
+    for ends, external in calls:
+        call, rows = W.call_subset(forest, ends, external)
+        tree = P.Tree.from_workload(call, opts=opts, device="cuda")
+        Q = torch.from_numpy(call.Q).to(dev).to(torch.bfloat16)
+        dO = torch.from_numpy(call.dO).to(dev).to(torch.bfloat16)
+        O, LSE = P.psattn_fwd(tree, Q, K, V)
+        dQ, _, _ = P.psattn_bwd(tree, Q, K, V, O, LSE, dO, dK=dK, dV=dV)
+        torch.cuda.synchronize()
+        Of[rows] = O.float().cpu().numpy()
+        LSEf[:, rows] = LSE.cpu().numpy()
+        dQf[rows] = dQ.cpu().numpy()
+    return Of, LSEf, dQf, dK.cpu().numpy().astype(np.float64), dV.cpu().numpy().astype(np.float64)
+
+
+def _compare(forest, got, ref):
+    t = forest.tree
+    slots = t.row_slots()
+    res = {}
+    for i, name in enumerate(("O", "LSE", "dQ")):
+        res[name] = H.compare(name, got[i], ref[i], "bf16")
+    for i, name in ((3, "dK"), (4, "dV")):
+        res[name] = H.compare(name, got[i][slots], ref[i][slots], "bf16")
+    return res
+
+
+FOREST = dict(parent=[-1, 0, 0, 1, 0, 1], seg=[300, 150, 70, 90, 20, 33], samples=[3, 2, 4, 5])
+
+
+@pytest.mark.parametrize("opts", [None, {"fwd_kv_split": 128, "bwd_q_chunk": 32}])
+def test_inter_batch_sharing(opts):
+    # call 1: the first sample's path (root, node 1, node 3); call 2: the other samples, with the
+    # nodes of call 1 cached
+    f = FOREST
+    forest = W.custom(f["parent"], f["seg"], f["samples"], hq=8, hkv=2, d=128, dtype="bf16", seed=31,
+                      block_policy=lambda L: W.blocks_fixed(L, 64))
+    t = forest.tree
+    first = [int(t.sample_end[0])]
+    done = set(m for e in first for m in t.path(e))
+    rest = [int(t.sample_end[s]) for s in range(1, len(t.sample_end))]
+    print(f"inter-batch: call 1 ends {first}, call 2 ends {rest} with {sorted(done)} cached", file=sys.stderr)
+    got = _run_calls(forest, [(first, []), (rest, sorted(done))], opts=opts)
+    res = _compare(forest, got, H.run_oracle(forest))
+    print(f"inter-batch {res}", file=sys.stderr)
+
+
+def test_three_micro_batches():
+    # one sample per call, each later call caching everything computed before it
+    f = FOREST
+    forest = W.custom(f["parent"], f["seg"], f["samples"], hq=10, hkv=2, d=128, dtype="bf16", seed=32,
+                      block_policy=W.blocks_exact)
+    t = forest.tree
+    calls, done = [], set()
+    for s in range(len(t.sample_end)):
+        e = int(t.sample_end[s])
+        calls.append(([e], sorted(done & set(t.path(e)))))
+        done |= set(t.path(e))
+    got = _run_calls(forest, calls)
+    res = _compare(forest, got, H.run_oracle(forest))
+    print(f"micro-batches {res}", file=sys.stderr)
+
+
+def test_self_sequence_sharing():
+    # one 900-token sequence as four chunks (a chain), one call per chunk: chunk c attends to the
+    # cached chunks 0..c-1 and adds to their dK/dV
+    forest = W.custom([-1, 0, 1, 2], [260, 230, 150, 260], [3], hq=8, hkv=2, d=64, dtype="bf16", seed=33,
+                      block_policy=W.blocks_greedy)
+    calls = [([c], list(range(c))) for c in range(4)]
+    got = _run_calls(forest, calls, opts={"bwd_q_chunk": 64})
+    res = _compare(forest, got, H.run_oracle(forest))
+    print(f"chunked {res}", file=sys.stderr)
