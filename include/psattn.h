@@ -181,6 +181,71 @@ psattn_status psattn_bwd_noalloc(const psattn_tree* tree, const void* Q, const v
                                  const void* O, const float* LSE, const void* dO,
                                  float* dQ, float* dK, float* dV, void* stream);
 
+/* ---- Adaptive KV cache manager (Sec. 5.1 adaptive block allocation, Sec. 5.2 dynamic block
+ * caching; Sec. 6 "Adaptive KV cache manager").  Host-only planning over a schedule of calls
+ * (micro-batches) on one pool of capacity_slots slots: which nodes each call computes (internal)
+ * and which it reads from the cache (external, psattn_tree_desc.row_off = -1), where each node's
+ * blocks lie, and the events the caller acts on.
+ *   - A node is stored when first needed: one block of exactly seg_len slots (block_size 0), or
+ *     ceil(seg_len / block_size) fixed pages.
+ *   - Reference count = samples that read the node.  After a call's backward it drops by the
+ *     call's samples that read it; with dbc at 0 the node is freed (PSATTN_KVM_FREE: its dK/dV
+ *     accumulators are complete).  Without dbc every block stays to the end of the schedule.
+ *   - When a block does not fit, cached nodes the call does not read are evicted, farthest next
+ *     use first (PSATTN_KVM_EVICT: flush the partial dK/dV accumulated so far, then the slots are
+ *     reused).  A later call that reads an evicted node gets it back in a new block
+ *     (PSATTN_KVM_REFILL: write its K/V there again and zero its dK/dV) as an external node.
+ *   - PSATTN_E_WORKSPACE when one call's own blocks do not fit in the pool. */
+typedef struct psattn_kvm psattn_kvm;
+typedef enum {
+  PSATTN_KVM_ALLOC = 0,   /* before the call: new block of a node the call computes */
+  PSATTN_KVM_REFILL = 1,  /* before the call: new block of an evicted node the call reads */
+  PSATTN_KVM_EVICT = 2,   /* before the call: block released while still to be read */
+  PSATTN_KVM_FREE = 3     /* after the call's backward: reference count 0, block released */
+} psattn_kvm_event_kind;
+typedef struct {
+  int32_t kind;        /* psattn_kvm_event_kind */
+  int32_t node;        /* forest node */
+  int32_t num_blocks;  /* blocks of the node (1, or its fixed pages) */
+  int32_t capacity;    /* slots of its first block */
+  int64_t base;        /* first slot of its first block */
+} psattn_kvm_event;
+typedef struct {
+  int64_t capacity_slots;  /* pool slots the manager allocates from (>= 1) */
+  int32_t block_size;      /* 0: adaptive, one block of exactly seg_len slots per node; > 0: fixed pages */
+  int32_t dbc;             /* 1: free a block at reference count 0; 0: keep every block to the end */
+  int32_t reserved[4];     /* must be 0 */
+} psattn_kvm_opts;
+typedef struct {
+  int64_t peak_slots;        /* most slots in use during any call */
+  int64_t final_slots;       /* slots still in use after the last call */
+  int64_t evictions;         /* blocks evicted before their last use */
+  int64_t refilled_tokens;   /* tokens written again after an eviction */
+  int64_t allocated_tokens;  /* tokens stored, first stores and refills */
+  int32_t num_calls;
+  int32_t pad_;
+} psattn_kvm_stats;
+
+/* Plan a schedule: the forest (parent / seg_len as in psattn_tree_desc) and, for each sample, its
+ * endpoint and the call that processes it (calls run in increasing index order; every index up
+ * to the largest holds a sample). */
+psattn_status psattn_kvm_plan(int32_t num_nodes, const int32_t* parent, const int32_t* seg_len,
+                              int32_t num_samples, const int32_t* sample_end, const int32_t* call_of_sample,
+                              const psattn_kvm_opts* opts, psattn_kvm** out);
+void psattn_kvm_destroy(psattn_kvm* kvm);
+/* The descriptor of one call: fills num_nodes, parent, seg_len, row_off (-1 for external nodes,
+ * internal rows packed in node order), blk_ptr, blocks, pool_slots and the samples; the caller
+ * sets hq, hkv, head_dim, softmax_scale, dtype.  node_ids (optional) maps the call's nodes to
+ * forest nodes.  Arrays stay valid until psattn_kvm_destroy. */
+psattn_status psattn_kvm_call_desc(const psattn_kvm* kvm, int32_t call, psattn_tree_desc* desc,
+                                   const int32_t** node_ids);
+/* The events of a call: phase 0 before it runs, 1 after its backward. */
+psattn_status psattn_kvm_events(const psattn_kvm* kvm, int32_t call, int32_t phase,
+                                const psattn_kvm_event** events, int32_t* count);
+/* Statistics; used_per_call (optional, num_calls entries) receives the slots in use during each
+ * call. */
+psattn_status psattn_kvm_get_stats(const psattn_kvm* kvm, psattn_kvm_stats* stats, int64_t* used_per_call);
+
 /* Reference count of every node: the number of samples whose path holds it
  * (Sec. 5.2).  node_refcount has num_nodes entries. */
 psattn_status psattn_tree_refcounts(const psattn_tree* tree, int32_t* node_refcount);

@@ -36,7 +36,10 @@ EXPORTED = [
     "psattn_tree_get_info",
     "psattn_tree_plan_array", "psattn_profile_enable", "psattn_profile_reset", "psattn_profile_read",
     "psattn_status_string", "psattn_last_error",
+    "psattn_kvm_plan", "psattn_kvm_destroy", "psattn_kvm_call_desc", "psattn_kvm_events", "psattn_kvm_get_stats",
 ]
+
+KVM_EVENTS = {0: "alloc", 1: "refill", 2: "evict", 3: "free"}
 
 PLAN_ARRAYS = {"row_pos": 0, "q_list": 1, "kv_list": 2, "fwd_items": 3, "fwd_merges": 4, "bkv_items": 5,
                "bkv_reduces": 6, "pad_slots": 7}
@@ -64,6 +67,22 @@ class TreeDesc(ctypes.Structure):
                 ("num_samples", ctypes.c_int32), ("sample_end", _i32p), ("hq", ctypes.c_int32),
                 ("hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
                 ("dtype", ctypes.c_int32)]
+
+
+class KvmEvent(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("node", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
+                ("capacity", ctypes.c_int32), ("base", ctypes.c_int64)]
+
+
+class KvmOpts(ctypes.Structure):
+    _fields_ = [("capacity_slots", ctypes.c_int64), ("block_size", ctypes.c_int32), ("dbc", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 4)]
+
+
+class KvmStats(ctypes.Structure):
+    _fields_ = [("peak_slots", ctypes.c_int64), ("final_slots", ctypes.c_int64), ("evictions", ctypes.c_int64),
+                ("refilled_tokens", ctypes.c_int64), ("allocated_tokens", ctypes.c_int64),
+                ("num_calls", ctypes.c_int32), ("pad_", ctypes.c_int32)]
 
 
 class PlanOpts(ctypes.Structure):
@@ -113,6 +132,14 @@ def lib() -> ctypes.CDLL:
         L.psattn_status_string.restype = ctypes.c_char_p
         L.psattn_last_error.argtypes = []
         L.psattn_last_error.restype = ctypes.c_char_p
+        L.psattn_kvm_plan.argtypes = [ctypes.c_int32, _i32p, _i32p, ctypes.c_int32, _i32p, _i32p,
+                                      ctypes.POINTER(KvmOpts), ctypes.POINTER(vp)]
+        L.psattn_kvm_destroy.argtypes = [vp]
+        L.psattn_kvm_destroy.restype = None
+        L.psattn_kvm_call_desc.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(TreeDesc), ctypes.POINTER(_i32p)]
+        L.psattn_kvm_events.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.POINTER(KvmEvent)),
+                                        _i32p]
+        L.psattn_kvm_get_stats.argtypes = [vp, ctypes.POINTER(KvmStats), _i64p]
         for name in EXPORTED:
             if name not in ("psattn_tree_destroy", "psattn_status_string", "psattn_last_error"):
                 getattr(L, name).restype = ctypes.c_int
@@ -333,6 +360,61 @@ def psattn_bwd_noalloc(tree: Tree, Q, K, V, O, LSE, dO, dQ, dK, dV):
     _check(lib().psattn_bwd_noalloc(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(dO), _vp(dQ), _vp(dK),
                                     _vp(dV), ctypes.c_void_p(stream)))
     return dQ, dK, dV
+
+
+class KVCachePlan:
+    """The adaptive KV cache manager's plan of a schedule (psattn_kvm_plan): a forest, the call
+    (micro-batch) of each sample, and a pool of ``capacity`` slots."""
+
+    def __init__(self, parent, seg_len, sample_end, call_of_sample, capacity, block_size=0, dbc=True):
+        L = lib()
+        self._handle = None
+        self.parent = np.ascontiguousarray(parent, dtype=np.int32)
+        self.seg_len = np.ascontiguousarray(seg_len, dtype=np.int32)
+        self.sample_end = np.ascontiguousarray(sample_end, dtype=np.int32)
+        self.call_of_sample = np.ascontiguousarray(call_of_sample, dtype=np.int32)
+        o = KvmOpts(int(capacity), int(block_size), 1 if dbc else 0)
+        h = ctypes.c_void_p()
+        _check(L.psattn_kvm_plan(len(self.parent), _ptr(self.parent, ctypes.c_int32), _ptr(self.seg_len, ctypes.c_int32),
+                                 len(self.sample_end), _ptr(self.sample_end, ctypes.c_int32),
+                                 _ptr(self.call_of_sample, ctypes.c_int32), ctypes.byref(o), ctypes.byref(h)))
+        self._handle = h
+        st = KvmStats()
+        _check(L.psattn_kvm_get_stats(h, ctypes.byref(st), None))
+        self.num_calls = st.num_calls
+        used = np.zeros(max(self.num_calls, 1), dtype=np.int64)
+        _check(L.psattn_kvm_get_stats(h, ctypes.byref(st), _ptr(used, ctypes.c_int64)))
+        self.stats = {k: getattr(st, k) for k, _ in KvmStats._fields_ if k != "pad_"}
+        self.used_per_call = used[:self.num_calls]
+
+    def __del__(self):
+        if getattr(self, "_handle", None) is not None:
+            lib().psattn_kvm_destroy(self._handle)
+            self._handle = None
+
+    def call(self, c: int) -> dict:
+        """Call c's descriptor arrays (numpy copies) and its forest node ids."""
+        d = TreeDesc()
+        ids = _i32p()
+        _check(lib().psattn_kvm_call_desc(self._handle, int(c), ctypes.byref(d), ctypes.byref(ids)))
+        n = d.num_nodes
+        nb = d.blk_ptr[n]
+        arr = lambda p, k: np.ctypeslib.as_array(p, shape=(k,)).copy() if k else np.zeros(0, dtype=np.int32)
+        blocks = [d.blocks[i] for i in range(nb)]
+        return {"node_ids": arr(ids, n), "parent": arr(d.parent, n), "seg_len": arr(d.seg_len, n),
+                "row_off": arr(d.row_off, n), "blk_ptr": arr(d.blk_ptr, n + 1),
+                "blk_base": np.array([b.base for b in blocks], dtype=np.int64),
+                "blk_cap": np.array([b.capacity for b in blocks], dtype=np.int32),
+                "blk_len": np.array([b.len for b in blocks], dtype=np.int32),
+                "blk_pos": np.array([b.pos for b in blocks], dtype=np.int32), "pool_slots": int(d.pool_slots),
+                "sample_end": arr(d.sample_end, d.num_samples)}
+
+    def events(self, c: int, phase: int) -> list:
+        """[(kind, forest node, num_blocks, capacity, base)] before (phase 0) or after (1) call c."""
+        ev = ctypes.POINTER(KvmEvent)()
+        n = ctypes.c_int32()
+        _check(lib().psattn_kvm_events(self._handle, int(c), int(phase), ctypes.byref(ev), ctypes.byref(n)))
+        return [(KVM_EVENTS[ev[i].kind], ev[i].node, ev[i].num_blocks, ev[i].capacity, ev[i].base) for i in range(n.value)]
 
 
 def psattn_profile_enable(on: bool = True) -> None:

@@ -99,3 +99,86 @@ def test_self_sequence_sharing():
     got = _run_calls(forest, calls, opts={"bwd_q_chunk": 64})
     res = _compare(forest, got, H.run_oracle(forest))
     print(f"chunked {res}", file=sys.stderr)
+
+
+def test_kv_cache_manager_schedule_with_eviction():
+    # the adaptive KV cache manager drives the calls: one sample per call, a pool too small to keep
+    # every shared block, so blocks are evicted (their partial dK/dV flushed) and refilled later
+    # (K/V written again, dK/dV restarted at zero); the flushed gradients of every node add up to
+    # the whole forest's dK/dV
+    import oracle as O
+    from paper_2608_25683_amd import psattn as P
+    forest = W.custom([-1, 0, 0, -1, 3, 3, 1], [200, 60, 90, 180, 40, 70, 50], [6, 2, 4, 5], hq=8, hkv=2, d=128,
+                      dtype="bf16", seed=41, block_policy=W.blocks_exact)
+    t = forest.tree
+    # calls: tree A (root 0) | tree B (root 3) | tree A again | tree B again; at call 2 only B's
+    # root can make room, although call 3 reads it
+    calls = [0, 2, 1, 3]
+    plan = P.KVCachePlan(t.parent, t.seg_len, t.sample_end, calls, capacity=420)
+    assert plan.stats["evictions"] >= 1 and plan.stats["refilled_tokens"] > 0
+    dev = torch.device("cuda")
+    cap, hkv, d = 420, forest.hkv, forest.d
+    Kp = torch.zeros((cap, hkv, d), dtype=torch.bfloat16, device=dev)
+    Vp = torch.zeros_like(Kp)
+    dK = torch.zeros((cap, hkv, d), dtype=torch.float32, device=dev)
+    dV = torch.zeros_like(dK)
+    Kt = torch.from_numpy(forest.K).to(dev).to(torch.bfloat16)     # node-packed (forest rows)
+    Vt = torch.from_numpy(forest.V).to(dev).to(torch.bfloat16)
+    slots_of = {}
+    gK = np.zeros((t.num_rows, hkv, d))
+    gV = np.zeros((t.num_rows, hkv, d))
+    Of = np.zeros((t.num_rows, forest.hq, d))
+    LSEf = np.zeros((forest.hq, t.num_rows))
+    dQf = np.zeros((t.num_rows, forest.hq, d))
+
+    def rows(n):
+        return np.arange(int(t.row_off[n]), int(t.row_off[n] + t.seg_len[n]))
+
+    def flush(n):
+        s = torch.from_numpy(slots_of[n]).to(dev)
+        gK[rows(n)] += dK[s].cpu().numpy()
+        gV[rows(n)] += dV[s].cpu().numpy()
+
+    for c in range(plan.num_calls):
+        x = plan.call(c)
+        for i, n in enumerate(x["node_ids"]):
+            sl = [np.arange(x["blk_base"][b], x["blk_base"][b] + x["blk_len"][b])
+                  for b in range(x["blk_ptr"][i], x["blk_ptr"][i + 1])]
+            new = np.concatenate(sl)
+            ev = {e[1]: e[0] for e in plan.events(c, 0)}
+            if ev.get(int(n)) in ("alloc", "refill"):
+                s = torch.from_numpy(new).to(dev)
+                r = torch.from_numpy(rows(int(n))).to(dev)
+                Kp[s] = Kt[r]
+                Vp[s] = Vt[r]
+                if ev[int(n)] == "refill":
+                    dK[s] = 0
+                    dV[s] = 0
+        for kind, n, _, _, _ in plan.events(c, 0):
+            if kind == "evict":
+                flush(n)
+        for i, n in enumerate(x["node_ids"]):
+            slots_of[int(n)] = np.concatenate([np.arange(x["blk_base"][b], x["blk_base"][b] + x["blk_len"][b])
+                                               for b in range(x["blk_ptr"][i], x["blk_ptr"][i + 1])])
+        tree = P.Tree(parent=x["parent"], seg_len=x["seg_len"], row_off=x["row_off"], blk_ptr=x["blk_ptr"],
+                      blk_base=x["blk_base"], blk_cap=x["blk_cap"], blk_len=x["blk_len"], blk_pos=x["blk_pos"],
+                      pool_slots=x["pool_slots"], sample_end=x["sample_end"], hq=forest.hq, hkv=hkv, head_dim=d,
+                      softmax_scale=forest.scale, device="cuda")
+        frows = np.concatenate([rows(int(n)) for i, n in enumerate(x["node_ids"]) if x["row_off"][i] >= 0])
+        Q = torch.from_numpy(forest.Q[frows]).to(dev).to(torch.bfloat16)
+        dO = torch.from_numpy(forest.dO[frows]).to(dev).to(torch.bfloat16)
+        Og, LSEg = P.psattn_fwd(tree, Q, Kp, Vp)
+        dQ, _, _ = P.psattn_bwd(tree, Q, Kp, Vp, Og, LSEg, dO, dK=dK, dV=dV)
+        torch.cuda.synchronize()
+        Of[frows] = Og.float().cpu().numpy()
+        LSEf[:, frows] = LSEg.cpu().numpy()
+        dQf[frows] = dQ.cpu().numpy()
+        for kind, n, _, _, _ in plan.events(c, 1):
+            if kind == "free":
+                flush(n)
+    Or, LSEr = O.forward(t.parent, t.seg_len, t.row_off, t.sample_end, forest.Q, forest.K, forest.V, forest.scale)
+    dQr, dKr, dVr = O.backward(t.parent, t.seg_len, t.row_off, t.sample_end, forest.Q, forest.K, forest.V, forest.dO,
+                               forest.scale)
+    res = {name: H.compare(name, g, r, "bf16") for name, g, r in
+           (("O", Of, Or), ("LSE", LSEf, LSEr), ("dQ", dQf, dQr), ("dK", gK, dKr), ("dV", gV, dVr))}
+    print(f"kv-cache schedule {plan.stats} {res}", file=sys.stderr)
