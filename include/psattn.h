@@ -246,6 +246,50 @@ psattn_status psattn_kvm_events(const psattn_kvm* kvm, int32_t call, int32_t pha
  * call. */
 psattn_status psattn_kvm_get_stats(const psattn_kvm* kvm, psattn_kvm_stats* stats, int64_t* used_per_call);
 
+/* ---- Host scheduling (Sec. 4.2 workload model and greedy placement, Sec. 4.3 token-wise
+ * micro-batching).  The workload of a sequence of length l whose first h tokens are cached is
+ * Eq. "single_sequence": T = a1 * l_suf * l + a2 * l_suf + a3, l_suf = l - h (attention, the
+ * per-token layers, a fixed overhead); alpha = (a1, a2, a3) from profiling. */
+
+/* Least-squares fit of alpha to n >= 3 measured runs (l_suf[i], l[i]) -> t[i]. */
+psattn_status psattn_sched_fit(int32_t n, const double* l_suf, const double* l, const double* t, double alpha[3]);
+/* Workload of each semantic group: the sum of T over its samples (in sample order), each counting
+ * as cached the nodes its group's earlier samples hold.  group_cost has num_groups entries. */
+psattn_status psattn_sched_group_costs(int32_t num_nodes, const int32_t* parent, const int32_t* seg_len,
+                                       int32_t num_samples, const int32_t* sample_end,
+                                       const int32_t* group_of_sample, int32_t num_groups,
+                                       const double alpha[3], double* group_cost);
+/* Greedy placement: groups in descending workload (ties by index), each whole onto the worker
+ * with the least load so far (ties: lowest index).  worker_load (optional) gets the loads. */
+psattn_status psattn_sched_place(int32_t num_groups, const double* group_cost, int32_t num_workers,
+                                 int32_t* worker_of_group, double* worker_load);
+/* Token-wise micro-batching of one worker's samples, in their order: budget = total workload /
+ * num_micro_batches; a sequence that would overflow the current micro-batch is cut at the token
+ * where it fills it, and its remaining tokens go on in the next micro-batch with the part done as
+ * cached prefix (the last micro-batch takes whatever remains).  The result is a refined forest in
+ * which every cut is a node boundary, and one chunk (a sample of the refined forest) per
+ * (sample, micro-batch) piece: ready for psattn_kvm_plan with call = micro-batch. */
+typedef struct psattn_sched_mb psattn_sched_mb;
+typedef struct {
+  int32_t num_nodes;                /* refined forest */
+  const int32_t* parent;
+  const int32_t* seg_len;
+  const int32_t* src_node;          /* original node of each refined node */
+  const int32_t* src_offset;        /* its first token within that node */
+  int32_t num_chunks;
+  const int32_t* chunk_end;         /* refined endpoint node of each chunk */
+  const int32_t* chunk_micro_batch; /* micro-batch of each chunk (0 .. num_micro_batches-1) */
+  const int32_t* chunk_sample;      /* original sample of each chunk */
+  int32_t num_micro_batches;        /* micro-batches that received work */
+  const double* micro_batch_cost;   /* estimated workload of each */
+} psattn_sched_mb_view;
+psattn_status psattn_sched_microbatch(int32_t num_nodes, const int32_t* parent, const int32_t* seg_len,
+                                      int32_t num_samples, const int32_t* sample_end, const double alpha[3],
+                                      int32_t num_micro_batches, psattn_sched_mb** out);
+/* Arrays stay valid until psattn_sched_mb_destroy. */
+psattn_status psattn_sched_mb_get(const psattn_sched_mb* mb, psattn_sched_mb_view* view);
+void psattn_sched_mb_destroy(psattn_sched_mb* mb);
+
 /* Reference count of every node: the number of samples whose path holds it
  * (Sec. 5.2).  node_refcount has num_nodes entries. */
 psattn_status psattn_tree_refcounts(const psattn_tree* tree, int32_t* node_refcount);

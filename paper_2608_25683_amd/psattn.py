@@ -37,6 +37,8 @@ EXPORTED = [
     "psattn_tree_plan_array", "psattn_profile_enable", "psattn_profile_reset", "psattn_profile_read",
     "psattn_status_string", "psattn_last_error",
     "psattn_kvm_plan", "psattn_kvm_destroy", "psattn_kvm_call_desc", "psattn_kvm_events", "psattn_kvm_get_stats",
+    "psattn_sched_fit", "psattn_sched_group_costs", "psattn_sched_place", "psattn_sched_microbatch",
+    "psattn_sched_mb_get", "psattn_sched_mb_destroy",
 ]
 
 KVM_EVENTS = {0: "alloc", 1: "refill", 2: "evict", 3: "free"}
@@ -83,6 +85,16 @@ class KvmStats(ctypes.Structure):
     _fields_ = [("peak_slots", ctypes.c_int64), ("final_slots", ctypes.c_int64), ("evictions", ctypes.c_int64),
                 ("refilled_tokens", ctypes.c_int64), ("allocated_tokens", ctypes.c_int64),
                 ("num_calls", ctypes.c_int32), ("pad_", ctypes.c_int32)]
+
+
+_f64p = ctypes.POINTER(ctypes.c_double)
+
+
+class SchedMbView(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_int32), ("parent", _i32p), ("seg_len", _i32p), ("src_node", _i32p),
+                ("src_offset", _i32p), ("num_chunks", ctypes.c_int32), ("chunk_end", _i32p),
+                ("chunk_micro_batch", _i32p), ("chunk_sample", _i32p), ("num_micro_batches", ctypes.c_int32),
+                ("micro_batch_cost", _f64p)]
 
 
 class PlanOpts(ctypes.Structure):
@@ -140,6 +152,15 @@ def lib() -> ctypes.CDLL:
         L.psattn_kvm_events.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.POINTER(KvmEvent)),
                                         _i32p]
         L.psattn_kvm_get_stats.argtypes = [vp, ctypes.POINTER(KvmStats), _i64p]
+        L.psattn_sched_fit.argtypes = [ctypes.c_int32, _f64p, _f64p, _f64p, _f64p]
+        L.psattn_sched_group_costs.argtypes = [ctypes.c_int32, _i32p, _i32p, ctypes.c_int32, _i32p, _i32p,
+                                               ctypes.c_int32, _f64p, _f64p]
+        L.psattn_sched_place.argtypes = [ctypes.c_int32, _f64p, ctypes.c_int32, _i32p, _f64p]
+        L.psattn_sched_microbatch.argtypes = [ctypes.c_int32, _i32p, _i32p, ctypes.c_int32, _i32p, _f64p,
+                                              ctypes.c_int32, ctypes.POINTER(vp)]
+        L.psattn_sched_mb_get.argtypes = [vp, ctypes.POINTER(SchedMbView)]
+        L.psattn_sched_mb_destroy.argtypes = [vp]
+        L.psattn_sched_mb_destroy.restype = None
         for name in EXPORTED:
             if name not in ("psattn_tree_destroy", "psattn_status_string", "psattn_last_error"):
                 getattr(L, name).restype = ctypes.c_int
@@ -415,6 +436,63 @@ class KVCachePlan:
         n = ctypes.c_int32()
         _check(lib().psattn_kvm_events(self._handle, int(c), int(phase), ctypes.byref(ev), ctypes.byref(n)))
         return [(KVM_EVENTS[ev[i].kind], ev[i].node, ev[i].num_blocks, ev[i].capacity, ev[i].base) for i in range(n.value)]
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def sched_fit(l_suf, l, t) -> np.ndarray:
+    """(a1, a2, a3) of Eq. "single_sequence" fitted to measured runs (psattn_sched_fit)."""
+    l_suf, l, t = _f64(l_suf), _f64(l), _f64(t)
+    alpha = np.zeros(3)
+    _check(lib().psattn_sched_fit(len(t), _ptr(l_suf, ctypes.c_double), _ptr(l, ctypes.c_double),
+                                  _ptr(t, ctypes.c_double), _ptr(alpha, ctypes.c_double)))
+    return alpha
+
+
+def sched_group_costs(parent, seg_len, sample_end, group_of_sample, num_groups, alpha) -> np.ndarray:
+    parent, seg_len, sample_end, gos, alpha = _i32(parent), _i32(seg_len), _i32(sample_end), _i32(group_of_sample), _f64(alpha)
+    out = np.zeros(int(num_groups))
+    _check(lib().psattn_sched_group_costs(len(parent), _ptr(parent, ctypes.c_int32), _ptr(seg_len, ctypes.c_int32),
+                                          len(sample_end), _ptr(sample_end, ctypes.c_int32), _ptr(gos, ctypes.c_int32),
+                                          int(num_groups), _ptr(alpha, ctypes.c_double), _ptr(out, ctypes.c_double)))
+    return out
+
+
+def sched_place(group_cost, num_workers):
+    """(worker of each group, load of each worker) of the greedy placement (psattn_sched_place)."""
+    c = _f64(group_cost)
+    w = np.zeros(len(c), dtype=np.int32)
+    load = np.zeros(int(num_workers))
+    _check(lib().psattn_sched_place(len(c), _ptr(c, ctypes.c_double), int(num_workers), _ptr(w, ctypes.c_int32),
+                                    _ptr(load, ctypes.c_double)))
+    return w, load
+
+
+def sched_microbatch(parent, seg_len, sample_end, alpha, num_micro_batches) -> dict:
+    """Token-wise micro-batching (psattn_sched_microbatch): the refined forest and its chunks."""
+    parent, seg_len, sample_end, alpha = _i32(parent), _i32(seg_len), _i32(sample_end), _f64(alpha)
+    h = ctypes.c_void_p()
+    L = lib()
+    _check(L.psattn_sched_microbatch(len(parent), _ptr(parent, ctypes.c_int32), _ptr(seg_len, ctypes.c_int32),
+                                     len(sample_end), _ptr(sample_end, ctypes.c_int32), _ptr(alpha, ctypes.c_double),
+                                     int(num_micro_batches), ctypes.byref(h)))
+    try:
+        v = SchedMbView()
+        _check(L.psattn_sched_mb_get(h, ctypes.byref(v)))
+        arr = lambda p, k, dt=np.int32: np.ctypeslib.as_array(p, shape=(k,)).astype(dt) if k else np.zeros(0, dt)
+        return {"parent": arr(v.parent, v.num_nodes), "seg_len": arr(v.seg_len, v.num_nodes),
+                "src_node": arr(v.src_node, v.num_nodes), "src_offset": arr(v.src_offset, v.num_nodes),
+                "chunk_end": arr(v.chunk_end, v.num_chunks), "chunk_micro_batch": arr(v.chunk_micro_batch, v.num_chunks),
+                "chunk_sample": arr(v.chunk_sample, v.num_chunks),
+                "micro_batch_cost": arr(v.micro_batch_cost, v.num_micro_batches, np.float64)}
+    finally:
+        L.psattn_sched_mb_destroy(h)
 
 
 def psattn_profile_enable(on: bool = True) -> None:

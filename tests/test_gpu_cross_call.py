@@ -101,26 +101,18 @@ def test_self_sequence_sharing():
     print(f"chunked {res}", file=sys.stderr)
 
 
-def test_kv_cache_manager_schedule_with_eviction():
-    # the adaptive KV cache manager drives the calls: one sample per call, a pool too small to keep
-    # every shared block, so blocks are evicted (their partial dK/dV flushed) and refilled later
-    # (K/V written again, dK/dV restarted at zero); the flushed gradients of every node add up to
-    # the whole forest's dK/dV
-    import oracle as O
+def _run_managed(forest, parent, seg_len, ends, calls, node_rows, capacity):
+    """Calls planned by the KV cache manager over a (possibly refined) forest whose node r holds the
+    forest rows node_rows(r); the test plays the caller: it writes K/V into new blocks, zeroes the
+    dK/dV of refilled ones, and flushes dK/dV of evicted and freed blocks into per-row sums."""
     from paper_2608_25683_amd import psattn as P
-    forest = W.custom([-1, 0, 0, -1, 3, 3, 1], [200, 60, 90, 180, 40, 70, 50], [6, 2, 4, 5], hq=8, hkv=2, d=128,
-                      dtype="bf16", seed=41, block_policy=W.blocks_exact)
+    plan = P.KVCachePlan(parent, seg_len, ends, calls, capacity=capacity)
     t = forest.tree
-    # calls: tree A (root 0) | tree B (root 3) | tree A again | tree B again; at call 2 only B's
-    # root can make room, although call 3 reads it
-    calls = [0, 2, 1, 3]
-    plan = P.KVCachePlan(t.parent, t.seg_len, t.sample_end, calls, capacity=420)
-    assert plan.stats["evictions"] >= 1 and plan.stats["refilled_tokens"] > 0
     dev = torch.device("cuda")
-    cap, hkv, d = 420, forest.hkv, forest.d
-    Kp = torch.zeros((cap, hkv, d), dtype=torch.bfloat16, device=dev)
+    hkv, d = forest.hkv, forest.d
+    Kp = torch.zeros((capacity, hkv, d), dtype=torch.bfloat16, device=dev)
     Vp = torch.zeros_like(Kp)
-    dK = torch.zeros((cap, hkv, d), dtype=torch.float32, device=dev)
+    dK = torch.zeros((capacity, hkv, d), dtype=torch.float32, device=dev)
     dV = torch.zeros_like(dK)
     Kt = torch.from_numpy(forest.K).to(dev).to(torch.bfloat16)     # node-packed (forest rows)
     Vt = torch.from_numpy(forest.V).to(dev).to(torch.bfloat16)
@@ -131,40 +123,34 @@ def test_kv_cache_manager_schedule_with_eviction():
     LSEf = np.zeros((forest.hq, t.num_rows))
     dQf = np.zeros((t.num_rows, forest.hq, d))
 
-    def rows(n):
-        return np.arange(int(t.row_off[n]), int(t.row_off[n] + t.seg_len[n]))
-
     def flush(n):
-        s = torch.from_numpy(slots_of[n]).to(dev)
-        gK[rows(n)] += dK[s].cpu().numpy()
-        gV[rows(n)] += dV[s].cpu().numpy()
+        s_ = torch.from_numpy(slots_of[n]).to(dev)
+        gK[node_rows(n)] += dK[s_].cpu().numpy()
+        gV[node_rows(n)] += dV[s_].cpu().numpy()
 
     for c in range(plan.num_calls):
         x = plan.call(c)
-        for i, n in enumerate(x["node_ids"]):
-            sl = [np.arange(x["blk_base"][b], x["blk_base"][b] + x["blk_len"][b])
-                  for b in range(x["blk_ptr"][i], x["blk_ptr"][i + 1])]
-            new = np.concatenate(sl)
-            ev = {e[1]: e[0] for e in plan.events(c, 0)}
-            if ev.get(int(n)) in ("alloc", "refill"):
-                s = torch.from_numpy(new).to(dev)
-                r = torch.from_numpy(rows(int(n))).to(dev)
-                Kp[s] = Kt[r]
-                Vp[s] = Vt[r]
-                if ev[int(n)] == "refill":
-                    dK[s] = 0
-                    dV[s] = 0
+        ev = {e[1]: e[0] for e in plan.events(c, 0)}
         for kind, n, _, _, _ in plan.events(c, 0):
             if kind == "evict":
                 flush(n)
         for i, n in enumerate(x["node_ids"]):
-            slots_of[int(n)] = np.concatenate([np.arange(x["blk_base"][b], x["blk_base"][b] + x["blk_len"][b])
-                                               for b in range(x["blk_ptr"][i], x["blk_ptr"][i + 1])])
+            new = np.concatenate([np.arange(x["blk_base"][b], x["blk_base"][b] + x["blk_len"][b])
+                                  for b in range(x["blk_ptr"][i], x["blk_ptr"][i + 1])])
+            if ev.get(int(n)) in ("alloc", "refill"):
+                s_ = torch.from_numpy(new).to(dev)
+                r = torch.from_numpy(node_rows(int(n))).to(dev)
+                Kp[s_] = Kt[r]
+                Vp[s_] = Vt[r]
+                if ev[int(n)] == "refill":
+                    dK[s_] = 0
+                    dV[s_] = 0
+            slots_of[int(n)] = new
         tree = P.Tree(parent=x["parent"], seg_len=x["seg_len"], row_off=x["row_off"], blk_ptr=x["blk_ptr"],
                       blk_base=x["blk_base"], blk_cap=x["blk_cap"], blk_len=x["blk_len"], blk_pos=x["blk_pos"],
                       pool_slots=x["pool_slots"], sample_end=x["sample_end"], hq=forest.hq, hkv=hkv, head_dim=d,
                       softmax_scale=forest.scale, device="cuda")
-        frows = np.concatenate([rows(int(n)) for i, n in enumerate(x["node_ids"]) if x["row_off"][i] >= 0])
+        frows = np.concatenate([node_rows(int(n)) for i, n in enumerate(x["node_ids"]) if x["row_off"][i] >= 0])
         Q = torch.from_numpy(forest.Q[frows]).to(dev).to(torch.bfloat16)
         dO = torch.from_numpy(forest.dO[frows]).to(dev).to(torch.bfloat16)
         Og, LSEg = P.psattn_fwd(tree, Q, Kp, Vp)
@@ -176,9 +162,53 @@ def test_kv_cache_manager_schedule_with_eviction():
         for kind, n, _, _, _ in plan.events(c, 1):
             if kind == "free":
                 flush(n)
+    return plan, (Of, LSEf, dQf, gK, gV)
+
+
+def _oracle_rows(forest):
+    import oracle as O
+    t = forest.tree
     Or, LSEr = O.forward(t.parent, t.seg_len, t.row_off, t.sample_end, forest.Q, forest.K, forest.V, forest.scale)
     dQr, dKr, dVr = O.backward(t.parent, t.seg_len, t.row_off, t.sample_end, forest.Q, forest.K, forest.V, forest.dO,
                                forest.scale)
-    res = {name: H.compare(name, g, r, "bf16") for name, g, r in
-           (("O", Of, Or), ("LSE", LSEf, LSEr), ("dQ", dQf, dQr), ("dK", gK, dKr), ("dV", gV, dVr))}
+    return Or, LSEr, dQr, dKr, dVr
+
+
+def _compare_rows(got, ref):
+    return {name: H.compare(name, g, r, "bf16") for name, g, r in zip(("O", "LSE", "dQ", "dK", "dV"), got, ref)}
+
+
+def test_kv_cache_manager_schedule_with_eviction():
+    # the adaptive KV cache manager drives the calls: one sample per call, a pool too small to keep
+    # every shared block, so a block is evicted (its partial dK/dV flushed) and refilled later
+    # (K/V written again, dK/dV restarted at zero); the flushed gradients of every node add up to
+    # the whole forest's dK/dV
+    forest = W.custom([-1, 0, 0, -1, 3, 3, 1], [200, 60, 90, 180, 40, 70, 50], [6, 2, 4, 5], hq=8, hkv=2, d=128,
+                      dtype="bf16", seed=41, block_policy=W.blocks_exact)
+    t = forest.tree
+    # calls: tree A (root 0) | tree B (root 3) | tree A again | tree B again; at call 2 only B's
+    # root can make room, although call 3 reads it
+    rows = lambda n: np.arange(int(t.row_off[n]), int(t.row_off[n] + t.seg_len[n]))
+    plan, got = _run_managed(forest, t.parent, t.seg_len, t.sample_end, [0, 2, 1, 3], rows, 420)
+    assert plan.stats["evictions"] >= 1 and plan.stats["refilled_tokens"] > 0
+    res = _compare_rows(got, _oracle_rows(forest))
     print(f"kv-cache schedule {plan.stats} {res}", file=sys.stderr)
+
+
+def test_token_wise_micro_batches():
+    # Sec. 4.3: the forest's samples cut into 5 micro-batches of near-equal Eq. 1 workload, long
+    # sequences split at token boundaries (the refined forest's nodes are pieces of the forest's);
+    # the KV cache manager plans the calls and the op runs them
+    from paper_2608_25683_amd import psattn as P
+    forest = W.custom([-1, 0, 0, 1, -1, 4], [700, 300, 120, 900, 250, 60], [3, 2, 5], hq=8, hkv=2, d=128,
+                      dtype="bf16", seed=43, block_policy=W.blocks_exact)
+    t = forest.tree
+    mb = P.sched_microbatch(t.parent, t.seg_len, t.sample_end, [2e-6, 3e-3, 0.5], 5)
+    assert len(mb["parent"]) > t.num_nodes      # some sequence was cut inside a node
+    rows = lambda r: np.arange(int(t.row_off[mb["src_node"][r]] + mb["src_offset"][r]),
+                               int(t.row_off[mb["src_node"][r]] + mb["src_offset"][r] + mb["seg_len"][r]))
+    plan, got = _run_managed(forest, mb["parent"], mb["seg_len"], mb["chunk_end"], mb["chunk_micro_batch"], rows,
+                             int(t.num_rows))
+    res = _compare_rows(got, _oracle_rows(forest))
+    print(f"micro-batches {len(mb['micro_batch_cost'])} calls, {len(mb['parent'])} refined nodes: {res}",
+          file=sys.stderr)
