@@ -290,6 +290,24 @@ psattn_status psattn_sched_microbatch(int32_t num_nodes, const int32_t* parent, 
 psattn_status psattn_sched_mb_get(const psattn_sched_mb* mb, psattn_sched_mb_view* view);
 void psattn_sched_mb_destroy(psattn_sched_mb* mb);
 
+/* ---- The rest of a layer in the shared layout (Sec. 6, prefix-sharing training runtime): the
+ * tree-dependent steps around the attention.  Each shared token has one sequence position (its
+ * block's pos), so every step below touches each shared row once. */
+
+/* Rotary position embedding in place: X [Ns][heads][d] of the given dtype (queries and keys in
+ * the tree's dtype, their fp32 gradients), row r at sequence position p(r): the pair
+ * (x_i, x_{i+d/2}), i < d/2, turns by p * theta^(-2i/d) (inverse != 0: by minus that, the
+ * transposed rotation for the backward).  theta > 1 (e.g. 10000). */
+psattn_status psattn_rope(const psattn_tree* tree, void* X, psattn_dtype dtype, int32_t heads, float theta,
+                          int32_t inverse, void* stream);
+/* K/V rows [Ns][Hkv][d] (the tree's dtype) written into their pool slots of K, V
+ * [pool_slots][Hkv][d]. */
+psattn_status psattn_kv_scatter(const psattn_tree* tree, const void* K_rows, const void* V_rows, void* K, void* V,
+                                void* stream);
+/* dK/dV of each row's pool slot, fp32 [pool_slots][Hkv][d] -> rows [Ns][Hkv][d]. */
+psattn_status psattn_kv_gather(const psattn_tree* tree, const float* dK, const float* dV, float* dK_rows,
+                               float* dV_rows, void* stream);
+
 /* Reference count of every node: the number of samples whose path holds it
  * (Sec. 5.2).  node_refcount has num_nodes entries. */
 psattn_status psattn_tree_refcounts(const psattn_tree* tree, int32_t* node_refcount);
@@ -305,6 +323,7 @@ psattn_status psattn_tree_get_info(const psattn_tree* tree, psattn_tree_info* in
  *   5 bkv_items [n][10]       kv_off nk kv_pos0 q_off nq hk part mask_lo mask_hi 0
  *   6 bkv_reduces [n][8]      kv_off nk hk part0 nparts 0 0 0
  *   7 pad_slots [n]           pool slots that hold no token
+ *   8 row_slot [Ns]           pool slot of each packed row's K/V
  * *data stays valid until psattn_tree_destroy. */
 psattn_status psattn_tree_plan_array(const psattn_tree* tree, int which, const int32_t** data,
                                      int64_t* count, int32_t* width);

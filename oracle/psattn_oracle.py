@@ -345,3 +345,113 @@ def keys_dkdv(ti: TreeIndex, Q, K, V, dO, scale, key_rows: Sequence[int], kv_hea
             dV[kidx] += p.T @ do
             dK[kidx] += scale * ((p * (dp - delta[:, None])).T @ q)
     return dK, dV
+
+
+# ----------------------------------------------------------------------------- one decoder layer
+#
+# The rest of a layer, written the same plain way: every sample expanded into its own sequence
+# and run through one decoder layer independently, gradients of duplicated tokens summed (Sec.
+# 2.5: shared results equal independent computation; Sec. 6: one backward over the accumulated
+# adjoints).  The layer: h = rmsnorm(x) g1; q, k, v = h Wq, h Wk, h Wv; rotary embedding of q and
+# k by sequence position; causal attention; y = x + o Wo; z = rmsnorm(y) g2;
+# out = y + (silu(z W1) * (z W3)) W2.  The loss of sample s is advantage-masked (Sec. 2.5):
+# L_s = A_s * sum_t m_{s,t} <c, out_{s,t}>, so each token counts only for the samples whose mask
+# holds it.
+
+def _rms(x, eps):
+    return np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+
+
+def _rope(x, pos, theta, sign=1.0):
+    """x [L, heads, d]: pairs (i, i + d/2) turned by sign * pos * theta^(-2i/d)."""
+    d = x.shape[-1]
+    half = d // 2
+    ang = sign * pos[:, None].astype(np.float64) * theta ** (-2.0 * np.arange(half) / d)[None, :]
+    c, s = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
+
+
+def layer_sample(x, pos, W, hq, hkv, scale, theta, eps, dout):
+    """One decoder layer on one sequence (fp64) and its backward for upstream gradient dout.
+
+    x [L, H]; pos [L]; W: g1, Wq, Wk, Wv, Wo, g2, W1, W3, W2.  Returns out [L, H], dx [L, H] and
+    the weight gradients (dict).
+    """
+    L = x.shape[0]
+    d = W["Wq"].shape[1] // hq
+    G = hq // hkv
+    r1 = _rms(x, eps)
+    h = x / r1 * W["g1"]
+    q = _rope((h @ W["Wq"]).reshape(L, hq, d), pos, theta)
+    k = _rope((h @ W["Wk"]).reshape(L, hkv, d), pos, theta)
+    v = (h @ W["Wv"]).reshape(L, hkv, d)
+    o = np.empty((L, hq, d))
+    lse = np.empty((hq, L))
+    for j in range(hq):
+        o[:, j], lse[j] = causal_fwd(q[:, j], k[:, j // G], v[:, j // G], scale)
+    y = x + o.reshape(L, hq * d) @ W["Wo"]
+    r2 = _rms(y, eps)
+    z = y / r2 * W["g2"]
+    a, b = z @ W["W1"], z @ W["W3"]
+    sig = 1.0 / (1.0 + np.exp(-a))
+    m = a * sig * b
+    out = y + m @ W["W2"]
+    # backward
+    g = {}
+    g["W2"] = m.T @ dout
+    dm = dout @ W["W2"].T
+    da = dm * b * (sig + a * sig * (1.0 - sig))
+    db = dm * a * sig
+    g["W1"], g["W3"] = z.T @ da, z.T @ db
+    dz = da @ W["W1"].T + db @ W["W3"].T
+    g["g2"] = np.sum(dz * y / r2, axis=0)
+    dzh = dz * W["g2"]
+    dy = dout + (dzh - (y / r2) * np.mean(dzh * y / r2, axis=-1, keepdims=True)) / r2
+    g["Wo"] = o.reshape(L, hq * d).T @ dy
+    do = (dy @ W["Wo"].T).reshape(L, hq, d)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for j in range(hq):
+        a_q, a_k, a_v = causal_bwd(q[:, j], k[:, j // G], v[:, j // G], o[:, j], lse[j], do[:, j], scale)
+        dq[:, j] += a_q
+        dk[:, j // G] += a_k
+        dv[:, j // G] += a_v
+    dq = _rope(dq, pos, theta, -1.0).reshape(L, hq * d)
+    dk = _rope(dk, pos, theta, -1.0).reshape(L, hkv * d)
+    dv = dv.reshape(L, hkv * d)
+    g["Wq"], g["Wk"], g["Wv"] = h.T @ dq, h.T @ dk, h.T @ dv
+    dh = dq @ W["Wq"].T + dk @ W["Wk"].T + dv @ W["Wv"].T
+    g["g1"] = np.sum(dh * x / r1, axis=0)
+    dhh = dh * W["g1"]
+    dx = dy + (dhh - (x / r1) * np.mean(dhh * x / r1, axis=-1, keepdims=True)) / r1
+    return out, dx, g
+
+
+def layer(parent, seg_len, row_off, sample_end, X, W, hq, hkv, scale, theta, eps, adv, loss_mask, c):
+    """The layer over a prefix forest, by expansion (fp64).
+
+    X [Ns, H] hidden state of every shared row; adv [S] advantage of each sample; loss_mask(s, rows)
+    -> 0/1 per position of sample s's sequence; c [H] the loss direction.  Returns out [Ns, H]
+    (checked equal on every copy of a shared token), dX [Ns, H] (duplicates summed) and the
+    weight gradients summed over samples.
+    """
+    X = _as64(X)
+    W = {k: _as64(v) for k, v in W.items()}
+    off = node_offsets(parent, seg_len)
+    out = np.full(X.shape, np.nan)
+    dX = np.zeros_like(X)
+    gW = {k: np.zeros_like(v) for k, v in W.items()}
+    for s, idx in enumerate(sample_rows(parent, seg_len, row_off, sample_end)):
+        pos = np.arange(len(idx))
+        dout = float(adv[s]) * np.asarray(loss_mask(s, idx), dtype=np.float64)[:, None] * _as64(c)[None, :]
+        o_s, dx_s, g_s = layer_sample(X[idx], pos, W, hq, hkv, scale, theta, eps, dout)
+        seen = ~np.isnan(out[idx, 0])
+        if np.any(seen):
+            assert np.max(np.abs(out[idx][seen] - o_s[seen])) <= 1e-9, "copies of a shared token differ"
+        out[idx] = o_s
+        np.add.at(dX, idx, dx_s)
+        for k in gW:
+            gW[k] += g_s[k]
+    return out, dX, gW

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpsattn.so")
-SOURCES = ["psattn_host.cpp", "psattn_kvcache.cpp", "psattn_sched.cpp", "psattn_fwd.hip", "psattn_bwd.hip", "psattn_noalloc.hip"]
+SOURCES = ["psattn_host.cpp", "psattn_kvcache.cpp", "psattn_sched.cpp", "psattn_fwd.hip", "psattn_bwd.hip", "psattn_layer.hip", "psattn_noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -60,14 +60,14 @@ struct psattn_tree {
   int64_t Ns = 0, Nu = 0, nvis = 0;
   // plan (host copy)
   Shape shape{};
-  std::vector<int32_t> row_pos, q_list, kv_list, pad_slots;
+  std::vector<int32_t> row_pos, row_slot, q_list, kv_list, pad_slots;
   std::vector<FwdItem> fwd;
   std::vector<MergeEntry> merge;
   std::vector<BkvItem> bkv;
   std::vector<ReduceEntry> reduce;
   int64_t fwd_part_rows = 0, bkv_part_tiles = 0;
   // device image of the plan
-  size_t o_row_pos = 0, o_q = 0, o_kv = 0, o_fwd = 0, o_merge = 0, o_bkv = 0, o_reduce = 0, o_pad = 0;
+  size_t o_row_pos = 0, o_row_slot = 0, o_q = 0, o_kv = 0, o_fwd = 0, o_merge = 0, o_bkv = 0, o_reduce = 0, o_pad = 0;
   size_t plan_bytes = 0;
   std::vector<uint8_t> image;
   void* dev = nullptr;
@@ -270,11 +270,15 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   // pool slots of every node's tokens, and sequence position of every packed row
   std::vector<std::vector<int32_t>> node_slots(N);
   t->row_pos.assign(t->Ns, 0);
+  t->row_slot.assign(t->Ns, 0);
   for (int n = 0; n < N; ++n) {
     for (int b = t->blk_ptr[n]; b < t->blk_ptr[n + 1]; ++b)
       for (int k = 0; k < t->blocks[b].len; ++k) node_slots[n].push_back((int32_t)(t->blocks[b].base + k));
     if (!t->ext[n])
-      for (int a = 0; a < t->seg_len[n]; ++a) t->row_pos[t->row_off[n] + a] = (int32_t)(t->off[n] + a);
+      for (int a = 0; a < t->seg_len[n]; ++a) {
+        t->row_pos[t->row_off[n] + a] = (int32_t)(t->off[n] + a);
+        t->row_slot[t->row_off[n] + a] = node_slots[n][a];
+      }
   }
 
   // per-node path slot list: slots of sequence positions 0 .. off+len-1
@@ -549,6 +553,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     return at;
   };
   t->o_row_pos = place(t->row_pos.size() * 4);
+  t->o_row_slot = place(t->row_slot.size() * 4);
   t->o_q = place(t->q_list.size() * 4);
   t->o_kv = place(t->kv_list.size() * 4);
   t->o_fwd = place(t->fwd.size() * sizeof(FwdItem));
@@ -562,6 +567,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     if (bytes) memcpy(t->image.data() + at, p, bytes);
   };
   put(t->o_row_pos, t->row_pos.data(), t->row_pos.size() * 4);
+  put(t->o_row_slot, t->row_slot.data(), t->row_slot.size() * 4);
   put(t->o_q, t->q_list.data(), t->q_list.size() * 4);
   put(t->o_kv, t->kv_list.data(), t->kv_list.size() * 4);
   put(t->o_fwd, t->fwd.data(), t->fwd.size() * sizeof(FwdItem));
@@ -576,6 +582,7 @@ PlanView plan_view(const psattn_tree* t) {
   const uint8_t* b = (const uint8_t*)t->dev;
   PlanView v;
   v.row_pos = (const int32_t*)(b + t->o_row_pos);
+  v.row_slot = (const int32_t*)(b + t->o_row_slot);
   v.q_list = (const int32_t*)(b + t->o_q);
   v.kv_list = (const int32_t*)(b + t->o_kv);
   v.fwd = (const FwdItem*)(b + t->o_fwd);
@@ -637,9 +644,9 @@ struct Profiler {
   std::vector<hipEvent_t> spare;
 };
 Profiler g_prof;
-const char* kKernelNames[] = {"fwd_main", "fwd_merge", "bwd_pre", "bwd_kv", "bwd_dq", "bwd_reduce_kv", "bwd_reduce_dq",
-                              "bwd_zero_pad"};
-constexpr int kNumKernels = 8;
+const char* kKernelNames[] = {"fwd_main", "fwd_merge",     "bwd_pre", "bwd_kv",   "bwd_dq", "bwd_reduce_kv",
+                              "bwd_reduce_dq", "bwd_zero_pad", "rope",    "kv_scatter", "kv_gather"};
+constexpr int kNumKernels = 11;
 
 hipEvent_t get_event() {
   if (!g_prof.spare.empty()) {
@@ -818,6 +825,47 @@ psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, con
   return s;
 }
 
+// ---------------------------------------------------------------------------------------------
+// Layer steps around the attention (the rest of a layer in the shared layout)
+
+psattn_status psattn_rope(const psattn_tree* t, void* X, psattn_dtype dtype, int32_t heads, float theta, int32_t inverse,
+                          void* stream) {
+  if (!t || !X) return fail(PSATTN_E_INVALID_ARG, "NULL argument");
+  if (dtype != PSATTN_BF16 && dtype != PSATTN_FP32) return fail(PSATTN_E_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+  if (!t->dev) return fail(PSATTN_E_NOT_UPLOADED, "call psattn_tree_upload before psattn_rope");
+  if (heads < 1) return fail(PSATTN_E_INVALID_ARG, "heads must be >= 1 (got %d)", heads);
+  if (!(theta > 1.f) || !std::isfinite(theta)) return fail(PSATTN_E_INVALID_ARG, "theta must be finite and > 1");
+  if (misaligned(X)) return fail(PSATTN_E_ALIGNMENT, "X must be 16-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  return timed(8, st, [&] {
+    return launch_rope(plan_view(t), (int32_t)t->Ns, heads, t->d, theta, inverse != 0, dtype == PSATTN_BF16, X, st);
+  });
+}
+
+psattn_status psattn_kv_scatter(const psattn_tree* t, const void* K_rows, const void* V_rows, void* K, void* V,
+                                void* stream) {
+  if (!t || !K_rows || !V_rows || !K || !V) return fail(PSATTN_E_INVALID_ARG, "NULL argument");
+  if (!t->dev) return fail(PSATTN_E_NOT_UPLOADED, "call psattn_tree_upload before psattn_kv_scatter");
+  if (misaligned(K_rows) || misaligned(V_rows) || misaligned(K) || misaligned(V))
+    return fail(PSATTN_E_ALIGNMENT, "tensor pointers must be 16-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  const int32_t row_bytes = t->hkv * t->d * (t->dtype == PSATTN_BF16 ? 2 : 4);
+  return timed(9, st, [&] { return launch_kv_move(plan_view(t), (int32_t)t->Ns, row_bytes, true, K_rows, V_rows, K, V, st); });
+}
+
+psattn_status psattn_kv_gather(const psattn_tree* t, const float* dK, const float* dV, float* dK_rows, float* dV_rows,
+                               void* stream) {
+  if (!t || !dK || !dV || !dK_rows || !dV_rows) return fail(PSATTN_E_INVALID_ARG, "NULL argument");
+  if (!t->dev) return fail(PSATTN_E_NOT_UPLOADED, "call psattn_tree_upload before psattn_kv_gather");
+  if (misaligned(dK) || misaligned(dV) || misaligned(dK_rows) || misaligned(dV_rows))
+    return fail(PSATTN_E_ALIGNMENT, "tensor pointers must be 16-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  const int32_t row_bytes = t->hkv * t->d * 4;
+  return timed(10, st, [&] {
+    return launch_kv_move(plan_view(t), (int32_t)t->Ns, row_bytes, false, dK, dV, dK_rows, dV_rows, st);
+  });
+}
+
 psattn_status psattn_tree_refcounts(const psattn_tree* t, int32_t* node_refcount) {
   if (!t || !node_refcount) return fail(PSATTN_E_INVALID_ARG, "NULL argument");
   std::copy(t->refcount.begin(), t->refcount.end(), node_refcount);
@@ -856,6 +904,7 @@ psattn_status psattn_tree_plan_array(const psattn_tree* t, int which, const int3
     case 5: *data = (const int32_t*)t->bkv.data(); *count = (int64_t)t->bkv.size(); *width = 10; break;
     case 6: *data = (const int32_t*)t->reduce.data(); *count = (int64_t)t->reduce.size(); *width = 8; break;
     case 7: *data = t->pad_slots.data(); *count = (int64_t)t->pad_slots.size(); *width = 1; break;
+    case 8: *data = t->row_slot.data(); *count = (int64_t)t->row_slot.size(); *width = 1; break;
     default: return fail(PSATTN_E_INVALID_ARG, "unknown plan array %d", which);
   }
   return PSATTN_OK;

@@ -1,4 +1,4 @@
-// Kernel launchers (defined in psattn_fwd.hip and psattn_bwd.hip, called by the C ABI).
+// Kernel launchers (defined in psattn_fwd.hip, psattn_bwd.hip and psattn_layer.hip, called by the C ABI).
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -54,5 +54,10 @@ hipError_t launch_bwd_dq(const BwdArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_bwd_reduce_kv(const BwdArgs& a, hipStream_t st);
 hipError_t launch_bwd_reduce_dq(const BwdArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_bwd_zero_pad(const BwdArgs& a, hipStream_t st);
+// layer steps around the attention (psattn_layer.hip)
+hipError_t launch_rope(const PlanView& plan, int32_t ns, int32_t heads, int32_t d, float theta, bool inverse, bool bf16,
+                       void* X, hipStream_t st);
+hipError_t launch_kv_move(const PlanView& plan, int32_t ns, int32_t row_bytes, bool to_pool, const void* a0,
+                          const void* a1, void* b0, void* b1, hipStream_t st);
 
 }  // namespace psattn

@@ -63,6 +63,7 @@ struct ReduceEntry {  // a key tile whose consumer rows were split into chunks
 // Device-side view of an uploaded plan.
 struct PlanView {
   const int32_t* row_pos;   // [Ns] sequence position of each packed row
+  const int32_t* row_slot;  // [Ns] pool slot of each packed row's K/V
   const int32_t* q_list;
   const int32_t* kv_list;
   const FwdItem* fwd;

@@ -38,13 +38,13 @@ EXPORTED = [
     "psattn_status_string", "psattn_last_error",
     "psattn_kvm_plan", "psattn_kvm_destroy", "psattn_kvm_call_desc", "psattn_kvm_events", "psattn_kvm_get_stats",
     "psattn_sched_fit", "psattn_sched_group_costs", "psattn_sched_place", "psattn_sched_microbatch",
-    "psattn_sched_mb_get", "psattn_sched_mb_destroy",
+    "psattn_sched_mb_get", "psattn_sched_mb_destroy", "psattn_rope", "psattn_kv_scatter", "psattn_kv_gather",
 ]
 
 KVM_EVENTS = {0: "alloc", 1: "refill", 2: "evict", 3: "free"}
 
 PLAN_ARRAYS = {"row_pos": 0, "q_list": 1, "kv_list": 2, "fwd_items": 3, "fwd_merges": 4, "bkv_items": 5,
-               "bkv_reduces": 6, "pad_slots": 7}
+               "bkv_reduces": 6, "pad_slots": 7, "row_slot": 8}
 
 
 class PsattnError(RuntimeError):
@@ -160,6 +160,9 @@ def lib() -> ctypes.CDLL:
                                               ctypes.c_int32, ctypes.POINTER(vp)]
         L.psattn_sched_mb_get.argtypes = [vp, ctypes.POINTER(SchedMbView)]
         L.psattn_sched_mb_destroy.argtypes = [vp]
+        L.psattn_rope.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_int32, vp]
+        L.psattn_kv_scatter.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.psattn_kv_gather.argtypes = [vp, vp, vp, vp, vp, vp]
         L.psattn_sched_mb_destroy.restype = None
         for name in EXPORTED:
             if name not in ("psattn_tree_destroy", "psattn_status_string", "psattn_last_error"):
@@ -493,6 +496,45 @@ def sched_microbatch(parent, seg_len, sample_end, alpha, num_micro_batches) -> d
                 "micro_batch_cost": arr(v.micro_batch_cost, v.num_micro_batches, np.float64)}
     finally:
         L.psattn_sched_mb_destroy(h)
+
+
+def psattn_rope(tree: Tree, X, theta: float = 10000.0, inverse: bool = False):
+    """Rotary embedding of X [Ns][heads][d] (bf16 or fp32) in place by each row's sequence position."""
+    import torch
+    if X.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("X must be bf16 or fp32")
+    _need(X, (tree.num_rows, X.shape[1], tree.head_dim), X.dtype, "X")
+    dt = PSATTN_BF16 if X.dtype == torch.bfloat16 else PSATTN_FP32
+    _check(lib().psattn_rope(tree.handle, _vp(X), dt, int(X.shape[1]), float(theta), 1 if inverse else 0,
+                             ctypes.c_void_p(torch.cuda.current_stream(X.device).cuda_stream)))
+    return X
+
+
+def psattn_kv_scatter(tree: Tree, K_rows, V_rows, K, V):
+    """K/V rows [Ns][Hkv][d] written into their pool slots of K, V."""
+    import torch
+    dt = _torch_dtype(tree)
+    for x, shape, name in ((K_rows, (tree.num_rows, tree.hkv, tree.head_dim), "K_rows"),
+                           (V_rows, (tree.num_rows, tree.hkv, tree.head_dim), "V_rows"),
+                           (K, (tree.pool_slots, tree.hkv, tree.head_dim), "K"),
+                           (V, (tree.pool_slots, tree.hkv, tree.head_dim), "V")):
+        _need(x, shape, dt, name)
+    _check(lib().psattn_kv_scatter(tree.handle, _vp(K_rows), _vp(V_rows), _vp(K), _vp(V),
+                                   ctypes.c_void_p(torch.cuda.current_stream(K.device).cuda_stream)))
+
+
+def psattn_kv_gather(tree: Tree, dK, dV, dK_rows=None, dV_rows=None):
+    """dK/dV of each row's pool slot -> rows [Ns][Hkv][d] (fp32)."""
+    import torch
+    shape = (tree.num_rows, tree.hkv, tree.head_dim)
+    dK_rows = torch.empty(shape, dtype=torch.float32, device=dK.device) if dK_rows is None else dK_rows
+    dV_rows = torch.empty(shape, dtype=torch.float32, device=dK.device) if dV_rows is None else dV_rows
+    for x, shp, name in ((dK, (tree.pool_slots,) + shape[1:], "dK"), (dV, (tree.pool_slots,) + shape[1:], "dV"),
+                         (dK_rows, shape, "dK_rows"), (dV_rows, shape, "dV_rows")):
+        _need(x, shp, torch.float32, name)
+    _check(lib().psattn_kv_gather(tree.handle, _vp(dK), _vp(dV), _vp(dK_rows), _vp(dV_rows),
+                                  ctypes.c_void_p(torch.cuda.current_stream(dK.device).cuda_stream)))
+    return dK_rows, dV_rows
 
 
 def psattn_profile_enable(on: bool = True) -> None:
