@@ -173,6 +173,8 @@ def main():
     dO = torch.from_numpy(wl.dO).to(dev).to(dt)
     ns, hq, hkv, d = tree.num_rows, wl.hq, wl.hkv, wl.d
     O_ = torch.empty((ns, hq, d), dtype=dt, device=dev)
+    # bf16: the forward also writes O's rounding residual, from which the backward takes Delta
+    O_lo = torch.empty_like(O_) if bf16 else None
     LSE = torch.empty((hq, ns), dtype=torch.float32, device=dev)
     dQ = torch.empty((ns, hq, d), dtype=torch.float32, device=dev)
     dK = torch.empty((tree.pool_slots, hkv, d), dtype=torch.float32, device=dev)
@@ -181,8 +183,8 @@ def main():
     ws_b = tree.workspace(1)
 
     def step():
-        P.psattn_fwd(tree, Q, K, V, O_, LSE, ws_f)
-        P.psattn_bwd(tree, Q, K, V, O_, LSE, dO, dQ, dK, dV, ws_b)
+        P.psattn_fwd(tree, Q, K, V, O_, LSE, ws_f, O_lo=O_lo)
+        P.psattn_bwd(tree, Q, K, V, O_, LSE, dO, dQ, dK, dV, ws_b, O_lo=O_lo)
 
     for _ in range(a.warmup):
         step()

@@ -152,19 +152,27 @@ psattn_status psattn_workspace_size(const psattn_tree* tree, int pass, size_t* b
  *   O[r][h]   = sum_j P_rj V[slot(j)][h/G],  P_r = softmax_j(scale * Q[r][h] . K[slot(j)][h/G])
  *   LSE[h][r] = log sum_j exp(scale * Q[r][h] . K[slot(j)][h/G])
  * over the keys j visible to row r.  Long key ranges may be split across
- * work items and merged by log-sum-exp.  ws may be NULL when its size is 0. */
+ * work items and merged by log-sum-exp.  ws may be NULL when its size is 0.
+ * O_lo (bf16 trees only, else NULL; optional, [Ns][Hq][d] like O, caller-owned):
+ * when given, it receives the rounding residual bf16(O_fp32 - O) of the fp32
+ * result, so that O + O_lo carries O to about 2^-16 relative.  psattn_bwd uses
+ * it for Delta (see there). */
 psattn_status psattn_fwd(const psattn_tree* tree, const void* Q, const void* K, const void* V,
-                         void* O, float* LSE, void* ws, size_t ws_bytes, void* stream);
+                         void* O, float* LSE, void* O_lo, void* ws, size_t ws_bytes, void* stream);
 
 /* Backward (Sec. 6: one backward pass over the accumulated adjoints).  dO is
  * the total adjoint of each shared token.  With P as above,
  * Delta_r = dO_r . O_r and dS = P * (dO V^T - Delta):
+ * (bf16: Delta_r = dO_r . (O_r + O_lo_r) when O_lo, the forward's residual, is
+ * given, else from the bf16 O alone.  Its error times sum_j P_rj K_j enters dQ,
+ * which matters on rows whose softmax sits on one large key; dK/dV use the
+ * exact sum_j P dP either way.)
  *   dQ = scale * dS K;  dK = scale * dS^T Q;  dV = P^T dO
  * where prefix dK/dV sum over every consuming branch and query head of the
  * group.  Partial sums are reduced in a fixed order (no floating-point
  * atomics): results are bitwise reproducible for a given tree and plan. */
 psattn_status psattn_bwd(const psattn_tree* tree, const void* Q, const void* K, const void* V,
-                         const void* O, const float* LSE, const void* dO,
+                         const void* O, const float* LSE, const void* O_lo, const void* dO,
                          float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes, void* stream);
 
 /* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
@@ -178,7 +186,7 @@ psattn_status psattn_bwd(const psattn_tree* tree, const void* Q, const void* K, 
  * each call writes every workspace byte it reads. */
 #define PSATTN_NOALLOC_SCRATCH_MIB 128
 psattn_status psattn_bwd_noalloc(const psattn_tree* tree, const void* Q, const void* K, const void* V,
-                                 const void* O, const float* LSE, const void* dO,
+                                 const void* O, const float* LSE, const void* O_lo, const void* dO,
                                  float* dQ, float* dK, float* dV, void* stream);
 
 /* ---- Adaptive KV cache manager (Sec. 5.1 adaptive block allocation, Sec. 5.2 dynamic block

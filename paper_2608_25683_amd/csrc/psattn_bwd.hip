@@ -1127,21 +1127,24 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   const int sub = threadIdx.x % lanes;
   float acc[PRE_PASSES];
   if (BF16) {
-    u32x4 x[PRE_PASSES], y[PRE_PASSES];
+    // O + O_lo (two bf16 whose fp32 sum is exact) when the forward's rounding residual is given
+    u32x4 x[PRE_PASSES], y[PRE_PASSES], z[PRE_PASSES];
+    const bool res = a.O_lo != nullptr;
 #pragma unroll
     for (int p = 0; p < PRE_PASSES; ++p) {
       const int row = min(row0 + p * per_pass, ns - 1);
       const size_t o = ((size_t)row * hq + h) * D + sub * 8;
       x[p] = ld16((const bf16_t*)a.O + o);
       y[p] = ld16((const bf16_t*)a.dO + o);
+      z[p] = res ? ld16((const bf16_t*)a.O_lo + o) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int p = 0; p < PRE_PASSES; ++p) {
       acc[p] = 0.f;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        acc[p] = fmaf(bf2f(x[p][e] & 0xffffu), bf2f(y[p][e] & 0xffffu), acc[p]);
-        acc[p] = fmaf(bf2f(x[p][e] >> 16), bf2f(y[p][e] >> 16), acc[p]);
+        acc[p] = fmaf(bf2f(x[p][e] & 0xffffu) + bf2f(z[p][e] & 0xffffu), bf2f(y[p][e] & 0xffffu), acc[p]);
+        acc[p] = fmaf(bf2f(x[p][e] >> 16) + bf2f(z[p][e] >> 16), bf2f(y[p][e] >> 16), acc[p]);
       }
     }
   } else {

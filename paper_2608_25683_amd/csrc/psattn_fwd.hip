@@ -403,28 +403,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
   // Unsplit items write O as whole rows: each wave stages its normalized bf16 rows in the LDS ring
   // (free once every wave has finished the PV products above; padded row stride OS), then copies
   // them out 16 bytes per lane, 1 KB of consecutive row bytes per instruction.  Row index and
-  // validity of staged row r come from lane r % 32 of the half that owns it.
+  // validity of staged row r come from lane r % 32 of the half that owns it.  With O_lo, a second
+  // round stages and writes the rounding residuals O - bf16(O) the same way.
   constexpr int OS = RB + 16;
   static_assert(NW * 32 * NH * OS <= NS * 2 * TB, "staged O rows fit the ring");
   const bool direct = it.part < 0;
   uint8_t* ot = &smem[0][0][0] + wave * (32 * NH) * OS;
-  if (direct) __syncthreads();
+  float inv[NH];
 #pragma unroll
   for (int rh = 0; rh < NH; ++rh) {
     const float l_tot = pair_sum(l_run[rh]);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    inv[rh] = l_tot > 0.f ? 1.f / l_tot : 0.f;
     const float lse = l_tot > 0.f ? m_run[rh] * a.s.scale + logf(l_tot) : kNegInf;
     if (direct) {
-      uint8_t* orow = ot + (32 * rh + l32) * OS;
-#pragma unroll
-      for (int mb = 0; mb < DB; ++mb)
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          u32x2 w;
-          w[0] = pack2(oacc[rh][mb][4 * g4 + 0] * inv, oacc[rh][mb][4 * g4 + 1] * inv);
-          w[1] = pack2(oacc[rh][mb][4 * g4 + 2] * inv, oacc[rh][mb][4 * g4 + 3] * inv);
-          *(u32x2*)(orow + 2 * (32 * mb + 8 * g4 + 4 * hh)) = w;
-        }
       if (row_ok[rh] && hh == 0) a.LSE[(size_t)head * a.s.ns + row[rh]] = lse;
       continue;
     }
@@ -437,23 +428,49 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4)
           *(f32x4*)(op + 32 * mb + 8 * g4 + 4 * hh) =
-              f32x4{oacc[rh][mb][4 * g4] * inv, oacc[rh][mb][4 * g4 + 1] * inv, oacc[rh][mb][4 * g4 + 2] * inv,
-                    oacc[rh][mb][4 * g4 + 3] * inv};
+              f32x4{oacc[rh][mb][4 * g4] * inv[rh], oacc[rh][mb][4 * g4 + 1] * inv[rh], oacc[rh][mb][4 * g4 + 2] * inv[rh],
+                    oacc[rh][mb][4 * g4 + 3] * inv[rh]};
       if (hh == 0) a.part_lse[prow * a.s.hq + head] = lse;
     }
   }
   if (direct) {
-    constexpr int CPRO = RB / 16, RPIO = 64 / CPRO;   // 16-byte chunks per row, rows per instruction
-    const int ch = lane % CPRO;
+    // round 0: bf16(O) into O; round 1: bf16(O - bf16(O)) into O_lo
+    auto write_rows = [&](bool lo, uint8_t* dst) __attribute__((always_inline)) {
 #pragma unroll
-    for (int k = 0; k < 32 * NH / RPIO; ++k) {
-      const int rl = k * RPIO + lane / CPRO;          // staged row; its half is (k * RPIO) / 32
-      const int rh = (k * RPIO) / 32;
-      const int r = __shfl(row[rh], rl % 32);
-      const int ok = __shfl((int)row_ok[rh], rl % 32);
-      const u32x4 v = *(const u32x4*)(ot + rl * OS + 16 * ch);
-      if (ok) *(u32x4*)((uint8_t*)a.O + ((size_t)r * a.s.hq + head) * RB + 16 * ch) = v;
-    }
+      for (int rh = 0; rh < NH; ++rh) {
+        uint8_t* orow = ot + (32 * rh + l32) * OS;
+#pragma unroll
+        for (int mb = 0; mb < DB; ++mb)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            float x[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              x[e] = oacc[rh][mb][4 * g4 + e] * inv[rh];
+              if (lo) x[e] -= bf2f(pack2(x[e], 0.f) & 0xffffu);
+            }
+            u32x2 w;
+            w[0] = pack2(x[0], x[1]);
+            w[1] = pack2(x[2], x[3]);
+            *(u32x2*)(orow + 2 * (32 * mb + 8 * g4 + 4 * hh)) = w;
+          }
+      }
+      constexpr int CPRO = RB / 16, RPIO = 64 / CPRO;   // 16-byte chunks per row, rows per instruction
+      const int ch = lane % CPRO;
+#pragma unroll
+      for (int k = 0; k < 32 * NH / RPIO; ++k) {
+        const int rl = k * RPIO + lane / CPRO;          // staged row; its half is (k * RPIO) / 32
+        const int rh = (k * RPIO) / 32;
+        const int r = __shfl(row[rh], rl % 32);
+        const int ok = __shfl((int)row_ok[rh], rl % 32);
+        const u32x4 v = *(const u32x4*)(ot + rl * OS + 16 * ch);
+        if (ok) *(u32x4*)(dst + ((size_t)r * a.s.hq + head) * RB + 16 * ch) = v;
+      }
+    };
+    __syncthreads();
+    write_rows(false, (uint8_t*)a.O);
+    // (the staging area is the wave's own: its LDS reads above complete before the writes below)
+    if (a.O_lo) write_rows(true, (uint8_t*)a.O_lo);
   }
 }
 
@@ -568,6 +585,12 @@ __global__ __launch_bounds__(256) void fwd_merge_kernel(FwdArgs a) {
       w2[0] = pack2(acc[0], acc[1]);
       w2[1] = pack2(acc[2], acc[3]);
       *(u32x2*)((bf16_t*)a.O + ((size_t)row * hq + h) * D + d4) = w2;
+      if (a.O_lo) {
+        u32x2 r2;
+        r2[0] = pack2(acc[0] - bf2f(w2[0] & 0xffffu), acc[1] - bf2f(w2[0] >> 16));
+        r2[1] = pack2(acc[2] - bf2f(w2[1] & 0xffffu), acc[3] - bf2f(w2[1] >> 16));
+        *(u32x2*)((bf16_t*)a.O_lo + ((size_t)row * hq + h) * D + d4) = r2;
+      }
     } else {
       *(f32x4*)((float*)a.O + ((size_t)row * hq + h) * D + d4) = acc;
     }

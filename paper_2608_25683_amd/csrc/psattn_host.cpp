@@ -741,12 +741,13 @@ psattn_status psattn_workspace_size(const psattn_tree* t, int pass, size_t* byte
   return PSATTN_OK;
 }
 
-psattn_status psattn_fwd(const psattn_tree* t, const void* Q, const void* K, const void* V, void* O, float* LSE, void* ws,
-                         size_t ws_bytes, void* stream) {
+psattn_status psattn_fwd(const psattn_tree* t, const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         void* O_lo, void* ws, size_t ws_bytes, void* stream) {
   if (!t) return fail(PSATTN_E_INVALID_ARG, "tree is NULL");
   if (!t->dev) return fail(PSATTN_E_NOT_UPLOADED, "call psattn_tree_upload before psattn_fwd");
   if (!Q || !K || !V || !O || !LSE) return fail(PSATTN_E_INVALID_ARG, "NULL tensor pointer");
-  if (misaligned(Q) || misaligned(K) || misaligned(V) || misaligned(O) || misaligned(LSE))
+  if (O_lo && t->dtype != PSATTN_BF16) return fail(PSATTN_E_INVALID_ARG, "O_lo is for bf16 trees only (must be NULL)");
+  if (misaligned(Q) || misaligned(K) || misaligned(V) || misaligned(O) || misaligned(LSE) || misaligned(O_lo))
     return fail(PSATTN_E_ALIGNMENT, "tensor pointers must be 16-byte aligned");
   FwdWs w = fwd_ws(t);
   if (ws_bytes < w.total || (w.total && !ws))
@@ -762,6 +763,7 @@ psattn_status psattn_fwd(const psattn_tree* t, const void* Q, const void* K, con
   a.K = K;
   a.V = V;
   a.O = O;
+  a.O_lo = O_lo;
   a.LSE = LSE;
   a.part_o = w.total ? (float*)((uint8_t*)ws + w.o_part_o) : nullptr;
   a.part_lse = w.total ? (float*)((uint8_t*)ws + w.o_part_lse) : nullptr;
@@ -773,13 +775,14 @@ psattn_status psattn_fwd(const psattn_tree* t, const void* Q, const void* K, con
 }
 
 psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, const void* V, const void* O,
-                         const float* LSE, const void* dO, float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes,
-                         void* stream) {
+                         const float* LSE, const void* O_lo, const void* dO, float* dQ, float* dK, float* dV, void* ws,
+                         size_t ws_bytes, void* stream) {
   if (!t) return fail(PSATTN_E_INVALID_ARG, "tree is NULL");
   if (!t->dev) return fail(PSATTN_E_NOT_UPLOADED, "call psattn_tree_upload before psattn_bwd");
   if (!Q || !K || !V || !O || !LSE || !dO || !dQ || !dK || !dV) return fail(PSATTN_E_INVALID_ARG, "NULL tensor pointer");
+  if (O_lo && t->dtype != PSATTN_BF16) return fail(PSATTN_E_INVALID_ARG, "O_lo is for bf16 trees only (must be NULL)");
   if (misaligned(Q) || misaligned(K) || misaligned(V) || misaligned(O) || misaligned(LSE) || misaligned(dO) ||
-      misaligned(dQ) || misaligned(dK) || misaligned(dV))
+      misaligned(dQ) || misaligned(dK) || misaligned(dV) || misaligned(O_lo))
     return fail(PSATTN_E_ALIGNMENT, "tensor pointers must be 16-byte aligned");
   BwdWs w = bwd_ws(t);
   if (!ws || ws_bytes < w.total)
@@ -798,6 +801,7 @@ psattn_status psattn_bwd(const psattn_tree* t, const void* Q, const void* K, con
   a.K = K;
   a.V = V;
   a.O = O;
+  a.O_lo = O_lo;
   a.LSE = LSE;
   a.dO = dO;
   a.dQ = dQ;

@@ -14,6 +14,7 @@ struct FwdArgs {
   const void* K;
   const void* V;
   void* O;
+  void* O_lo;       // bf16: residual O - bf16(O) of the fp32 result [Ns][Hq][d], or null
   float* LSE;
   float* part_o;    // [partial rows][Hq][d]
   float* part_lse;  // [partial rows][Hq]
@@ -28,6 +29,7 @@ struct BwdArgs {
   const void* K;
   const void* V;
   const void* O;
+  const void* O_lo; // bf16: residual of O (Delta from O + O_lo), or null
   const float* LSE;
   const void* dO;
   float* dQ;

@@ -50,8 +50,8 @@ psattn_status scratch_ptr(void** out) {
 }  // namespace
 
 extern "C" psattn_status psattn_bwd_noalloc(const psattn_tree* tree, const void* Q, const void* K, const void* V,
-                                            const void* O, const float* LSE, const void* dO, float* dQ, float* dK,
-                                            float* dV, void* stream) {
+                                            const void* O, const float* LSE, const void* O_lo, const void* dO,
+                                            float* dQ, float* dK, float* dV, void* stream) {
   size_t need = 0;
   psattn_status st = psattn_workspace_size(tree, 1, &need);
   if (st != PSATTN_OK) return st;
@@ -64,5 +64,5 @@ extern "C" psattn_status psattn_bwd_noalloc(const psattn_tree* tree, const void*
   void* ws = nullptr;
   st = scratch_ptr(&ws);
   if (st != PSATTN_OK) return st;
-  return psattn_bwd(tree, Q, K, V, O, LSE, dO, dQ, dK, dV, ws, kScratchBytes, stream);
+  return psattn_bwd(tree, Q, K, V, O, LSE, O_lo, dO, dQ, dK, dV, ws, kScratchBytes, stream);
 }

@@ -68,14 +68,15 @@ class SharedLayer:
         P.psattn_rope(tree, q, self.theta)
         P.psattn_rope(tree, k, self.theta)
         P.psattn_kv_scatter(tree, k, v, K_pool, V_pool)
-        o, lse = P.psattn_fwd(tree, q, K_pool, V_pool)
+        o_lo = torch.empty_like(q) if dt == torch.bfloat16 else None   # O's rounding residual (Delta)
+        o, lse = P.psattn_fwd(tree, q, K_pool, V_pool, O_lo=o_lo)
         y = X + o.view(ns, hq * d) @ W["Wo"]
         r2 = self._rms(y)
         z = (y.float() * r2).to(dt) * W["g2"]
         a, b = z @ W["W1"], z @ W["W3"]
         m = torch.nn.functional.silu(a) * b
         out = y + m @ W["W2"]
-        saved = dict(X=X, r1=r1, h=h, q=q, o=o, lse=lse, y=y, r2=r2, z=z, a=a, b=b, m=m, K=K_pool, V=V_pool)
+        saved = dict(X=X, r1=r1, h=h, q=q, o=o, o_lo=o_lo, lse=lse, y=y, r2=r2, z=z, a=a, b=b, m=m, K=K_pool, V=V_pool)
         return out, saved
 
     def backward(self, tree: P.Tree, saved, dout):
@@ -102,7 +103,7 @@ class SharedLayer:
         o = s["o"]
         g["Wo"] = f(o.view(ns, hq * d)).t() @ dy
         do = (dy @ f(W["Wo"]).t()).view(ns, hq, d).to(o.dtype).contiguous()
-        dq, dKp, dVp = P.psattn_bwd(tree, s["q"], s["K"], s["V"], o, s["lse"], do)
+        dq, dKp, dVp = P.psattn_bwd(tree, s["q"], s["K"], s["V"], o, s["lse"], do, O_lo=s["o_lo"])
         dk, dv = P.psattn_kv_gather(tree, dKp, dVp)
         P.psattn_rope(tree, dq, self.theta, inverse=True)
         P.psattn_rope(tree, dk, self.theta, inverse=True)

@@ -7,8 +7,8 @@ the call raises.
 
 Names follow the C ABI in include/psattn.h:
     Tree(...)                       psattn_tree_create / _upload / _destroy
-    psattn_fwd(tree, Q, K, V)       -> (O, LSE)
-    psattn_bwd(tree, Q, K, V, O, LSE, dO) -> (dQ, dK, dV)
+    psattn_fwd(tree, Q, K, V)       -> (O, LSE)   (O_lo=: the bf16 rounding residual of O)
+    psattn_bwd(tree, Q, K, V, O, LSE, dO) -> (dQ, dK, dV)   (O_lo=: Delta from O + O_lo)
 """
 from __future__ import annotations
 
@@ -130,9 +130,9 @@ def lib() -> ctypes.CDLL:
         L.psattn_tree_device_bytes.argtypes = [vp, ctypes.POINTER(sz)]
         L.psattn_tree_upload.argtypes = [vp, vp, sz, vp]
         L.psattn_workspace_size.argtypes = [vp, ctypes.c_int, ctypes.POINTER(sz)]
-        L.psattn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
-        L.psattn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
-        L.psattn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.psattn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.psattn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.psattn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.psattn_tree_refcounts.argtypes = [vp, _i32p]
         L.psattn_tree_get_info.argtypes = [vp, ctypes.POINTER(TreeInfo)]
         L.psattn_tree_plan_array.argtypes = [vp, ctypes.c_int, ctypes.POINTER(_i32p), _i64p, _i32p]
@@ -312,8 +312,9 @@ def _vp(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-def psattn_fwd(tree: Tree, Q, K, V, O=None, LSE=None, ws=None):
-    """Forward pass on the current stream; returns (O [Ns,Hq,d], LSE [Hq,Ns] fp32)."""
+def psattn_fwd(tree: Tree, Q, K, V, O=None, LSE=None, ws=None, O_lo=None):
+    """Forward pass on the current stream; returns (O [Ns,Hq,d], LSE [Hq,Ns] fp32).  O_lo (bf16
+    trees, optional, like O): filled with the rounding residual of O, for psattn_bwd."""
     import torch
     if tree._plan_buf is None:
         raise RuntimeError("tree not uploaded (call Tree.upload)")
@@ -328,16 +329,19 @@ def psattn_fwd(tree: Tree, Q, K, V, O=None, LSE=None, ws=None):
         LSE = torch.empty((hq, ns), dtype=torch.float32, device=Q.device)
     _need(O, (ns, hq, d), dt, "O")
     _need(LSE, (hq, ns), torch.float32, "LSE")
+    if O_lo is not None:
+        _need(O_lo, (ns, hq, d), dt, "O_lo")
     if ws is None:
         ws = tree.workspace(0)
     stream = torch.cuda.current_stream(Q.device).cuda_stream
-    _check(lib().psattn_fwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(ws), ws.numel(),
+    _check(lib().psattn_fwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(O_lo), _vp(ws), ws.numel(),
                             ctypes.c_void_p(stream)))
     return O, LSE
 
 
-def psattn_bwd(tree: Tree, Q, K, V, O, LSE, dO, dQ=None, dK=None, dV=None, ws=None):
-    """Backward pass on the current stream; returns (dQ, dK, dV), all fp32."""
+def psattn_bwd(tree: Tree, Q, K, V, O, LSE, dO, dQ=None, dK=None, dV=None, ws=None, O_lo=None):
+    """Backward pass on the current stream; returns (dQ, dK, dV), all fp32.  O_lo: the forward's
+    residual of O, if it was produced (Delta then comes from O + O_lo)."""
     import torch
     if tree._plan_buf is None:
         raise RuntimeError("tree not uploaded (call Tree.upload)")
@@ -349,6 +353,8 @@ def psattn_bwd(tree: Tree, Q, K, V, O, LSE, dO, dQ=None, dK=None, dV=None, ws=No
     _need(O, (ns, hq, d), dt, "O")
     _need(LSE, (hq, ns), torch.float32, "LSE")
     _need(dO, (ns, hq, d), dt, "dO")
+    if O_lo is not None:
+        _need(O_lo, (ns, hq, d), dt, "O_lo")
     f32 = torch.float32
     if dQ is None:
         dQ = torch.empty((ns, hq, d), dtype=f32, device=Q.device)
@@ -362,12 +368,12 @@ def psattn_bwd(tree: Tree, Q, K, V, O, LSE, dO, dQ=None, dK=None, dV=None, ws=No
     if ws is None:
         ws = tree.workspace(1)
     stream = torch.cuda.current_stream(Q.device).cuda_stream
-    _check(lib().psattn_bwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(dO), _vp(dQ), _vp(dK),
-                            _vp(dV), _vp(ws), ws.numel(), ctypes.c_void_p(stream)))
+    _check(lib().psattn_bwd(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(O_lo), _vp(dO), _vp(dQ),
+                            _vp(dK), _vp(dV), _vp(ws), ws.numel(), ctypes.c_void_p(stream)))
     return dQ, dK, dV
 
 
-def psattn_bwd_noalloc(tree: Tree, Q, K, V, O, LSE, dO, dQ, dK, dV):
+def psattn_bwd_noalloc(tree: Tree, Q, K, V, O, LSE, dO, dQ, dK, dV, O_lo=None):
     """psattn_bwd with its workspace in the library's per-GPU device array (no workspace argument,
     nothing allocated by the library); the output tensors are the caller's."""
     import torch
@@ -380,9 +386,11 @@ def psattn_bwd_noalloc(tree: Tree, Q, K, V, O, LSE, dO, dQ, dK, dV):
                               (O, (ns, hq, d), dt, "O"), (LSE, (hq, ns), f32, "LSE"), (dO, (ns, hq, d), dt, "dO"),
                               (dQ, (ns, hq, d), f32, "dQ"), (dK, (ps, hkv, d), f32, "dK"), (dV, (ps, hkv, d), f32, "dV")):
         _need(x, shape, t, name)
+    if O_lo is not None:
+        _need(O_lo, (ns, hq, d), dt, "O_lo")
     stream = torch.cuda.current_stream(Q.device).cuda_stream
-    _check(lib().psattn_bwd_noalloc(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(dO), _vp(dQ), _vp(dK),
-                                    _vp(dV), ctypes.c_void_p(stream)))
+    _check(lib().psattn_bwd_noalloc(tree.handle, _vp(Q), _vp(K), _vp(V), _vp(O), _vp(LSE), _vp(O_lo), _vp(dO),
+                                    _vp(dQ), _vp(dK), _vp(dV), ctypes.c_void_p(stream)))
     return dQ, dK, dV
 
 

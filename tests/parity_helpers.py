@@ -9,8 +9,9 @@ from paper_2608_25683_amd import workloads as W
 TOL = {"bf16": (2e-2, 5e-3), "fp32": (1e-5, 1e-5)}   # (max-abs, relative L2) per output tensor
 
 
-def run_gpu(wl, opts=None, reps=1):
-    """Forward + backward through the C ABI; returns float64 numpy outputs (dK/dV in pool layout)."""
+def run_gpu(wl, opts=None, reps=1, residual=True):
+    """Forward + backward through the C ABI; returns float64 numpy outputs (dK/dV in pool layout).
+    bf16: with residual, the forward's rounding residual of O goes to the backward (O_lo)."""
     import torch
     from paper_2608_25683_amd import psattn as P
     tree = P.Tree.from_workload(wl, opts=opts, device="cuda")
@@ -19,10 +20,11 @@ def run_gpu(wl, opts=None, reps=1):
     K = torch.from_numpy(wl.K_pool).to("cuda").to(dt)
     V = torch.from_numpy(wl.V_pool).to("cuda").to(dt)
     dO = torch.from_numpy(wl.dO).to("cuda").to(dt)
+    O_lo = torch.empty_like(Q) if (residual and wl.dtype == "bf16") else None
     outs = []
     for _ in range(reps):
-        Og, LSEg = P.psattn_fwd(tree, Q, K, V)
-        dQ, dK, dV = P.psattn_bwd(tree, Q, K, V, Og, LSEg, dO)
+        Og, LSEg = P.psattn_fwd(tree, Q, K, V, O_lo=O_lo)
+        dQ, dK, dV = P.psattn_bwd(tree, Q, K, V, Og, LSEg, dO, O_lo=O_lo)
         torch.cuda.synchronize()
         outs.append(tuple(x.float().cpu().numpy().astype(np.float64) for x in (Og, LSEg, dQ, dK, dV)))
     return outs if reps > 1 else outs[0]

@@ -127,7 +127,7 @@ def test_opts_reserved_must_be_zero(base):
 def test_calls_before_upload_fail(base):
     t = _make(**base)
     L = P.lib()
-    st = L.psattn_fwd(t.handle, *(ctypes.c_void_p(64),) * 5, None, 0, None)
+    st = L.psattn_fwd(t.handle, *(ctypes.c_void_p(64),) * 5, None, None, 0, None)
     assert P.STATUS[st] == "PSATTN_E_NOT_UPLOADED"
     st = L.psattn_workspace_size(t.handle, 2, ctypes.byref(ctypes.c_size_t()))
     assert P.STATUS[st] == "PSATTN_E_INVALID_ARG"

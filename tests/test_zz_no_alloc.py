@@ -18,7 +18,7 @@ def test_noalloc_rejects_a_workspace_beyond_its_array():
                   block_policy=W.blocks_exact)
     tree = P.Tree.from_workload(wl)
     assert tree.workspace_size(1) > (P.NOALLOC_SCRATCH_MIB << 20)
-    null = [None] * 9
+    null = [None] * 10
     st = P.lib().psattn_bwd_noalloc(tree.handle, *null, None)
     assert P.STATUS[st] == "PSATTN_E_WORKSPACE"
     assert b"psattn_bwd_noalloc holds" in P.lib().psattn_last_error()
@@ -37,10 +37,11 @@ def test_noalloc_matches_bwd_on_two_calls():
         sizes.append(tree.workspace_size(1))
         dev = torch.device("cuda")
         Q, K, V, dO = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (wl.Q, wl.K_pool, wl.V_pool, wl.dO))
-        Og, LSEg = P.psattn_fwd(tree, Q, K, V)
-        ref = P.psattn_bwd(tree, Q, K, V, Og, LSEg, dO)
+        O_lo = torch.empty_like(Q)
+        Og, LSEg = P.psattn_fwd(tree, Q, K, V, O_lo=O_lo)
+        ref = P.psattn_bwd(tree, Q, K, V, Og, LSEg, dO, O_lo=O_lo)
         out = [torch.full_like(x, float("nan")) for x in ref]
-        P.psattn_bwd_noalloc(tree, Q, K, V, Og, LSEg, dO, *out)
+        P.psattn_bwd_noalloc(tree, Q, K, V, Og, LSEg, dO, *out, O_lo=O_lo)
         torch.cuda.synchronize()
         for name, a, b in zip(("dQ", "dK", "dV"), ref, out):
             assert torch.equal(a, b), f"{name}: psattn_bwd_noalloc differs from psattn_bwd"
