@@ -1115,15 +1115,16 @@ __global__ __launch_bounds__(512) void bwd_dq_f32_kernel(BwdArgs a) {
 // D/8 lanes per (row, head), 8 elements each.  A workgroup takes PRE_PASSES x (256 / (D/8))
 // consecutive rows of one head, so the per-head statistics ([head][row]) are written as
 // contiguous runs; every lane issues all its loads before the first product.
+// (row, head) pairs in memory order (O, dO and O_lo are [Ns][Hq][d]): D/8 lanes per pair, 8
+// elements each, so that every pass of a workgroup reads one contiguous span of each tensor
 constexpr int PRE_PASSES = 4;
 template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   const int D = a.s.d, hq = a.s.hq, ns = a.s.ns;
   const int lanes = D / 8;
   const int per_pass = 256 / lanes;
-  const int blocks_per_head = (ns + per_pass * PRE_PASSES - 1) / (per_pass * PRE_PASSES);
-  const int h = blockIdx.x / blocks_per_head;
-  const int row0 = (blockIdx.x % blocks_per_head) * per_pass * PRE_PASSES + threadIdx.x / lanes;
+  const int64_t npairs = (int64_t)ns * hq;
+  const int64_t pair0 = (int64_t)blockIdx.x * per_pass * PRE_PASSES + threadIdx.x / lanes;
   const int sub = threadIdx.x % lanes;
   float acc[PRE_PASSES];
   if (BF16) {
@@ -1132,8 +1133,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
     const bool res = a.O_lo != nullptr;
 #pragma unroll
     for (int p = 0; p < PRE_PASSES; ++p) {
-      const int row = min(row0 + p * per_pass, ns - 1);
-      const size_t o = ((size_t)row * hq + h) * D + sub * 8;
+      const size_t o = (size_t)min(pair0 + p * per_pass, npairs - 1) * D + sub * 8;
       x[p] = ld16((const bf16_t*)a.O + o);
       y[p] = ld16((const bf16_t*)a.dO + o);
       z[p] = res ? ld16((const bf16_t*)a.O_lo + o) : u32x4{0u, 0u, 0u, 0u};
@@ -1151,8 +1151,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
     f32x4 x[PRE_PASSES][2], y[PRE_PASSES][2];
 #pragma unroll
     for (int p = 0; p < PRE_PASSES; ++p) {
-      const int row = min(row0 + p * per_pass, ns - 1);
-      const size_t o = ((size_t)row * hq + h) * D + sub * 8;
+      const size_t o = (size_t)min(pair0 + p * per_pass, npairs - 1) * D + sub * 8;
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         x[p][k] = *(const f32x4*)((const float*)a.O + o + 4 * k);
@@ -1171,8 +1170,9 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 #pragma unroll
   for (int p = 0; p < PRE_PASSES; ++p) {
     for (int w = lanes / 2; w >= 1; w >>= 1) acc[p] += __shfl_xor(acc[p], w);
-    const int row = row0 + p * per_pass;
-    if (row < ns && sub == 0) {
+    const int64_t pr = pair0 + p * per_pass;
+    if (pr < npairs && sub == 0) {
+      const int row = (int)(pr / hq), h = (int)(pr % hq);
       const size_t o = (size_t)h * ns + row;
       const float lse = a.LSE[o];
       a.delta[o] = acc[p];
@@ -1248,9 +1248,8 @@ __global__ __launch_bounds__(256) void bwd_zero_pad_kernel(BwdArgs a) {
 }  // namespace
 
 hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16, hipStream_t st) {
-  const int rows_per_block = 256 / (a.s.d / 8) * PRE_PASSES;
-  const int64_t blocks_per_head = ((int64_t)a.s.ns + rows_per_block - 1) / rows_per_block;
-  const dim3 grid((unsigned)(blocks_per_head * a.s.hq));
+  const int pairs_per_block = 256 / (a.s.d / 8) * PRE_PASSES;
+  const dim3 grid((unsigned)(((int64_t)a.s.ns * a.s.hq + pairs_per_block - 1) / pairs_per_block));
   if (bf16) hipLaunchKernelGGL((bwd_pre_kernel<true>), grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL((bwd_pre_kernel<false>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
