@@ -253,16 +253,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
   };
   // remainder products of one step, if any of its P > 2^-9 or |dS| > 2^-5 (wave-uniform branch):
-  // Pf/Sf its fp32 P and dS, Ph/Sh their packed bf16, Qs/dOs its ring slot
+  // Pf/Sf its fp32 P and dS, Ph/Sh their packed bf16, Qs/dOs its ring slot.  The maxima are
+  // eight steps each: step k of the P maximum takes elements {0, 1, 2}, then {2k+1, 2k+2}, then
+  // {15}; step k of the |dS| maximum takes {2k, 2k+1}.
   constexpr float kRemP = 1.0f / 512, kRemS = 1.0f / 32;
-  auto remainders = [&](const f32x16& Pf, const f32x16& Sf, const bf16x8 (&Ph)[2], const bf16x8 (&Sh)[2], uint32_t Qs,
-                        uint32_t dOs) __attribute__((always_inline)) {
-    float mp = max3f(Pf[0], Pf[1], Pf[2]), ms = max3abs(0.f, Sf[0], Sf[1]);
-#pragma unroll
-    for (int v = 3; v < 15; v += 2) mp = max3f(mp, Pf[v], Pf[v + 1]);
-    mp = max2f(mp, Pf[15]);
-#pragma unroll
-    for (int v = 2; v < 16; v += 2) ms = max3abs(ms, Sf[v], Sf[v + 1]);
+  auto max_p_step = [&](float& mp, const f32x16& Pf, int k) __attribute__((always_inline)) {
+    if (k == 0) mp = max3f(Pf[0], Pf[1], Pf[2]);
+    else if (k < 7) mp = max3f(mp, Pf[2 * k + 1], Pf[2 * k + 2]);
+    else mp = max2f(mp, Pf[15]);
+  };
+  auto max_s_step = [&](float& ms, const f32x16& Sf, int k) __attribute__((always_inline)) {
+    ms = max3abs(k == 0 ? 0.f : ms, Sf[2 * k], Sf[2 * k + 1]);
+  };
+  auto rem_apply = [&](float mp, float ms, const f32x16& Pf, const f32x16& Sf, const bf16x8 (&Ph)[2],
+                       const bf16x8 (&Sh)[2], uint32_t Qs, uint32_t dOs) __attribute__((always_inline)) {
     if (__builtin_amdgcn_ballot_w64(mp > kRemP || ms > kRemS) == 0) return;
     bf16x8 pl[2], sl[2];
 #pragma unroll
@@ -279,6 +283,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       mma_a(dv[nb], pl[t2], ld_t(dOs, u));
       mma_a(dk[nb], sl[t2], ld_t(Qs, u));
     }
+  };
+  auto remainders = [&](const f32x16& Pf, const f32x16& Sf, const bf16x8 (&Ph)[2], const bf16x8 (&Sh)[2], uint32_t Qs,
+                        uint32_t dOs) __attribute__((always_inline)) {
+    float mp = 0.f, ms = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      max_p_step(mp, Pf, k);
+      max_s_step(ms, Sf, k);
+    }
+    rem_apply(mp, ms, Pf, Sf, Ph, Sh, Qs, dOs);
   };
   int h3, subc;                               // head of the copy step i+3 and subtile of min(i+3, nsteps-1)
   int h0 = 0, sub0 = 0;                       // head and subtile of step i
@@ -351,12 +365,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
       });
     };
+    // the remainder test of step i-1 runs alongside its dV/dK pairs: the maxima of its fp32 P (in
+    // Sn) and dS (in dPn) take one step per MFMA slot, the P maximum after the dV MFMAs and the
+    // |dS| maximum after the dK MFMAs; the ballot and the remainder products follow the last pair
+    float rem_p = 0.f, rem_s = 0.f;
     auto slot = [&](auto ic) __attribute__((always_inline)) {
       constexpr int si = decltype(ic)::value;
       constexpr int m = si / 2, w = si % 2;
       if constexpr (si == 0) mask_s(Sc, i, sub0);
       if constexpr (REM && si == 2 * NT) {   // before the statistics pair overwrites Sn / dPn
-        remainders(Sn, dPn, Pp, Sp, Qp, dOp);
+        rem_apply(rem_p, rem_s, Sn, dPn, Pp, Sp, Qp, dOp);
         sched_fence();
       }
       if constexpr (w == 0) load_frag(m + PF);
@@ -373,6 +391,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         else mma_v(dPn, fo[s], vreg[s]);
       }
       chunk(ic);
+      if constexpr (REM && m < NT) {
+        static_for<8 / NT + (8 % NT ? 1 : 0)>([&](auto jc) __attribute__((always_inline)) {
+          constexpr int k = m * 8 / NT + decltype(jc)::value;
+          if constexpr (k < (m + 1) * 8 / NT) {
+            if constexpr (w == 0) {
+              max_p_step(rem_p, Sn, k);
+              anchor(rem_p);
+            } else {
+              max_s_step(rem_s, dPn, k);
+              anchor(rem_s);
+            }
+          }
+        });
+      }
       if constexpr (si == BAR) {
         wait_vmem<(NR - 4) * (CPS + 1)>();
         if (new_blk) wait_lds<0>();   // the staged row block is written before the barrier
@@ -732,6 +764,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
         if constexpr (F(e) + 2 == q) {
           dPc[rh][v] = Sc[rh][v] * dPc[rh][v];
           eps[rh] += dPc[rh][v];
+          anchor(eps[rh]);   // (else the compiler gathers the 32 dependent adds in one block)
         }
         if constexpr (v % 8 == 7 && F(e) + 2 == q) {
           dSc[rh][v / 8] = pack8(dPc[rh], 8 * (v / 8));
