@@ -69,7 +69,8 @@ typedef enum {
   PSATTN_E_WORKSPACE = -7,       /* workspace or plan buffer too small */
   PSATTN_E_ALIGNMENT = -8,       /* device pointer not 16-byte aligned */
   PSATTN_E_HIP = -9,             /* a HIP runtime call failed (message has the HIP error) */
-  PSATTN_E_NOT_UPLOADED = -10    /* psattn_fwd/bwd called before psattn_tree_upload */
+  PSATTN_E_NOT_UPLOADED = -10,   /* psattn_fwd/bwd called before psattn_tree_upload */
+  PSATTN_E_INTERNAL = -11        /* plan consistency check failed (builds with PSATTN_PLAN_CHECKS) */
 } psattn_status;
 
 typedef enum { PSATTN_BF16 = 0, PSATTN_FP32 = 1 } psattn_dtype;

@@ -247,6 +247,59 @@ std::vector<int> longest_first(const std::vector<double>& cost) {
   return ord;
 }
 
+#ifdef PSATTN_PLAN_CHECKS
+// Opt-in (-DPSATTN_PLAN_CHECKS): every index the kernels derive from the plan lies inside the
+// array or buffer it addresses -- row and slot lists, item ranges, partial rows and tiles.  The
+// sanitized host build of the tests compiles it in.
+psattn_status check_plan(const psattn_tree* t) {
+  const int64_t nql = (int64_t)t->q_list.size(), nkl = (int64_t)t->kv_list.size();
+  const int64_t ns = t->shape.ns, slots = t->pool_slots;
+  auto bad = [&](const char* what, int64_t i) {
+    return fail(PSATTN_E_INTERNAL, "plan check: %s (entry %lld)", what, (long long)i);
+  };
+  for (int64_t i = 0; i < ns; ++i) {
+    if (t->row_pos[i] < 0) return bad("row position < 0", i);
+    if (t->row_slot[i] < 0 || t->row_slot[i] >= slots) return bad("row slot outside the pool", i);
+  }
+  for (int64_t i = 0; i < nql; ++i)
+    if (t->q_list[i] < 0 || t->q_list[i] >= ns) return bad("q_list row outside [0, Ns)", i);
+  for (int64_t i = 0; i < nkl; ++i)
+    if (t->kv_list[i] < 0 || t->kv_list[i] >= slots) return bad("kv_list slot outside the pool", i);
+  for (size_t i = 0; i < t->pad_slots.size(); ++i)
+    if (t->pad_slots[i] < 0 || t->pad_slots[i] >= slots) return bad("pad slot outside the pool", (int64_t)i);
+  const Shape& s = t->shape;
+  for (size_t i = 0; i < t->fwd.size(); ++i) {
+    const FwdItem& f = t->fwd[i];
+    if (f.nq < 1 || f.nq > s.bmq || f.q_off < 0 || (int64_t)f.q_off + f.nq > nql) return bad("forward item rows", (int64_t)i);
+    if (f.nkv < 1 || f.kv_off < 0 || (int64_t)f.kv_off + f.nkv > nkl) return bad("forward item keys", (int64_t)i);
+    if (f.head0 < 0 || f.head0 + s.hc > s.hq || f.head0 / s.g != (f.head0 + s.hc - 1) / s.g) return bad("forward item heads", (int64_t)i);
+    if (f.part < -1 || (f.part >= 0 && (int64_t)f.part + f.nq > t->fwd_part_rows)) return bad("forward item partial rows", (int64_t)i);
+    if (f.nfull < 0 || (int64_t)f.nfull * KV_TILE > f.nkv + KV_TILE - 1) return bad("forward item unmasked tiles", (int64_t)i);
+  }
+  for (size_t i = 0; i < t->merge.size(); ++i) {
+    const MergeEntry& m = t->merge[i];
+    if (m.nq < 1 || m.q_off < 0 || (int64_t)m.q_off + m.nq > nql) return bad("merge rows", (int64_t)i);
+    if (m.nparts < 1 || m.part0 < 0 || (int64_t)m.part0 + (int64_t)(m.nparts - 1) * s.bmq + m.nq > t->fwd_part_rows)
+      return bad("merge partial rows", (int64_t)i);
+  }
+  for (size_t i = 0; i < t->bkv.size(); ++i) {
+    const BkvItem& b = t->bkv[i];
+    if (b.nk < 1 || b.nk > BKV_TILE || b.kv_off < 0 || (int64_t)b.kv_off + b.nk > nkl) return bad("dK/dV item keys", (int64_t)i);
+    if (b.nq < 1 || b.q_off < 0 || (int64_t)b.q_off + b.nq > nql) return bad("dK/dV item rows", (int64_t)i);
+    if (b.hk < 0 || b.hk >= s.hkv) return bad("dK/dV item kv head", (int64_t)i);
+    if (b.part < -1 || b.part >= t->bkv_part_tiles) return bad("dK/dV item partial tile", (int64_t)i);
+    if (b.mask_lo < 0 || b.mask_lo > b.mask_hi || b.mask_hi > b.nq) return bad("dK/dV item mask range", (int64_t)i);
+  }
+  for (size_t i = 0; i < t->reduce.size(); ++i) {
+    const ReduceEntry& r = t->reduce[i];
+    if (r.nk < 1 || r.nk > BKV_TILE || r.kv_off < 0 || (int64_t)r.kv_off + r.nk > nkl) return bad("reduce keys", (int64_t)i);
+    if (r.hk < 0 || r.hk >= s.hkv) return bad("reduce kv head", (int64_t)i);
+    if (r.nparts < 1 || r.part0 < 0 || (int64_t)r.part0 + r.nparts > t->bkv_part_tiles) return bad("reduce partial tiles", (int64_t)i);
+  }
+  return PSATTN_OK;
+}
+#endif
+
 psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   const int N = t->N;
   Shape& s = t->shape;
@@ -698,6 +751,9 @@ psattn_status psattn_tree_create(const psattn_tree_desc* desc, const psattn_plan
   try {
     st = validate_and_copy(desc, t);
     if (st == PSATTN_OK) st = build_plan(t, o);
+#ifdef PSATTN_PLAN_CHECKS
+    if (st == PSATTN_OK) st = check_plan(t);
+#endif
   } catch (const std::bad_alloc&) {
     st = fail(PSATTN_E_UNSUPPORTED, "out of host memory while planning");
   } catch (...) {
@@ -968,6 +1024,7 @@ const char* psattn_status_string(psattn_status s) {
     case PSATTN_E_ALIGNMENT: return "PSATTN_E_ALIGNMENT";
     case PSATTN_E_HIP: return "PSATTN_E_HIP";
     case PSATTN_E_NOT_UPLOADED: return "PSATTN_E_NOT_UPLOADED";
+    case PSATTN_E_INTERNAL: return "PSATTN_E_INTERNAL";
   }
   return "PSATTN_E_UNKNOWN";
 }

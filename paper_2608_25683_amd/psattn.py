@@ -28,6 +28,7 @@ STATUS = {
     0: "PSATTN_OK", -1: "PSATTN_E_INVALID_ARG", -2: "PSATTN_E_INVALID_TREE", -3: "PSATTN_E_BLOCK_RANGE",
     -4: "PSATTN_E_BLOCK_OVERLAP", -5: "PSATTN_E_BLOCK_COVERAGE", -6: "PSATTN_E_UNSUPPORTED",
     -7: "PSATTN_E_WORKSPACE", -8: "PSATTN_E_ALIGNMENT", -9: "PSATTN_E_HIP", -10: "PSATTN_E_NOT_UPLOADED",
+    -11: "PSATTN_E_INTERNAL",
 }
 
 EXPORTED = [

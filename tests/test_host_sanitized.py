@@ -7,6 +7,9 @@ with -fsanitize=address,undefined and no recovery from undefined behaviour, and 
 (descriptor validation, random-forest planner coverage, packing and split plans, cross-call
 plans, the KV cache manager, the scheduler) run against that build in a child process.  Any
 out-of-bounds access, use after free or signed overflow in validation or planning fails here.
+The build also turns on PSATTN_PLAN_CHECKS: every plan is checked so that each index the kernels
+derive from it (row and slot lists, item ranges, partial rows and tiles) lies inside what it
+addresses, or tree creation fails with PSATTN_E_INTERNAL.
 """
 import os
 import shutil
@@ -27,7 +30,7 @@ def _runtime(name):
 @pytest.mark.skipif(shutil.which("g++") is None or _runtime("libasan.so") is None, reason="needs g++ with libasan")
 def test_host_abi_tests_pass_under_asan_and_ubsan(tmp_path):
     lib = str(tmp_path / "libpsattn_host_sanitized.so")
-    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-shared", "-fsanitize=address,undefined",
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-shared", "-fsanitize=address,undefined", "-DPSATTN_PLAN_CHECKS",
            "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer",
            "-I", os.path.join(ROOT, "tests", "sanitize"), "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(CSRC, "psattn_host.cpp"), os.path.join(CSRC, "psattn_kvcache.cpp"),
