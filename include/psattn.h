@@ -333,6 +333,7 @@ psattn_status psattn_tree_get_info(const psattn_tree* tree, psattn_tree_info* in
  *   6 bkv_reduces [n][8]      kv_off nk hk part0 nparts 0 0 0
  *   7 pad_slots [n]           pool slots that hold no token
  *   8 row_slot [Ns]           pool slot of each packed row's K/V
+ *   9 q_pos                   sequence position of each q_list entry
  * *data stays valid until psattn_tree_destroy. */
 psattn_status psattn_tree_plan_array(const psattn_tree* tree, int which, const int32_t** data,
                                      int64_t* count, int32_t* width);

@@ -81,16 +81,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int crow = lane / CPR, cpc = lane % CPR;
   const uint32_t kv_stride = (uint32_t)(a.s.hkv * D * sizeof(bf16_t));
 
-  {
-    const int r = ql[min(tid, nq - 1)];
-    s_row[0][tid] = r;
-    s_qpos[0][tid] = tid < nq ? a.plan.row_pos[r] : -1;
-  }
-  int pre_row = 0, pre_qpos = -1;
-  if (nq > IDX_BLK) {
-    pre_row = ql[min(IDX_BLK + tid, nq - 1)];
-    pre_qpos = IDX_BLK + tid < nq ? a.plan.row_pos[pre_row] : -1;
-  }
+  // consumer rows staged 256 at a time: row index (past the list: the last row again) and
+  // sequence position (past the list: -1, the q_pos entry before the array).  Block 0 here; block
+  // B >= 1 by LDS-DMA two iterations before its first copy step (see the iteration)
+  const int* qp = a.plan.q_pos + it.q_off;
+  s_row[0][tid] = ql[min(tid, nq - 1)];
+  s_qpos[0][tid] = tid < nq ? qp[tid] : -1;
+  auto stage_block = [&](int blk) __attribute__((always_inline)) {
+    const int e = blk * IDX_BLK + tid;
+    copy4_to_lds(ql + min(e, nq - 1), &s_row[blk & 1][64 * wave]);
+    copy4_to_lds(e < nq ? qp + e : a.plan.q_pos - 1, &s_qpos[blk & 1][64 * wave]);
+  };
   // K and V rows of this wave's keys: B operands (lane <-> key, 8 consecutive head_dim entries
   // per k-slot)
   bf16x8 kreg[KS], vreg[KS];
@@ -136,17 +137,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   };
   const uint32_t nd_dist = (uint32_t)((const char*)a.kv_nd - (const char*)a.kv_nls);
   const uint32_t row_bytes = (uint32_t)hq * RB;
-  auto fetch_rows = [&](int sub) __attribute__((always_inline)) {   // rows of subtile sub (staged)
+  // rows of subtile sub (staged): the LDS reads, then the offsets (split, so that the reads can be
+  // issued well before their results are needed)
+  struct RowIdx {
+    int r[CPS + 1];
+  };
+  auto read_rows = [&](int sub) __attribute__((always_inline)) {
     const int* rows = &s_row[0][0] + (sub & 15) * Q_SUB;
+    RowIdx x;
+#pragma unroll
+    for (int j = 0; j < CPS; ++j) x.r[j] = rows[((wave + 4 * j) % NI) * RPI + crow];
+    x.r[CPS] = rows[lane >> 1];
+    return x;
+  };
+  auto row_offsets = [&](const RowIdx& x) __attribute__((always_inline)) {
     Rows o;
 #pragma unroll
     for (int j = 0; j < CPS; ++j) {
       const int r = ((wave + 4 * j) % NI) * RPI + crow;
-      o.off[j] = (uint32_t)rows[r] * row_bytes + ((cpc ^ swz<D>(r)) << 4);
+      o.off[j] = (uint32_t)x.r[j] * row_bytes + ((cpc ^ swz<D>(r)) << 4);
     }
-    o.st = (uint32_t)rows[lane >> 1] * 4 + ((lane & 1) ? nd_dist : 0u);
+    o.st = (uint32_t)x.r[CPS] * 4 + ((lane & 1) ? nd_dist : 0u);
     return o;
   };
+  auto fetch_rows = [&](int sub) __attribute__((always_inline)) { return row_offsets(read_rows(sub)); };
   const void* gsrc[CPS];                      // tensor of copy j
   uint32_t gdst[CPS];                         // its LDS byte offset within a ring slot
 #pragma unroll
@@ -221,7 +235,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr int BAR = 2 * (NT - PF) - 1 < 3 ? 2 * (NT - PF) - 1 : 3;
   constexpr int CP0 = BAR + 1, CPD = 3;       // copy j of step i+3 at slot CP0 + CPD*j
   constexpr int ST_SLOT = CP0 + CPD * CPS, ROW_SLOT = ST_SLOT + 2;
-  static_assert(BAR >= 1 && ROW_SLOT < NSLOT && 2 * (NT - PF) > BAR, "iteration schedule");
+  static_assert(BAR >= 1 && ROW_SLOT < NSLOT && 2 * (NT - PF) > BAR && ROW_SLOT > BAR + 1, "iteration schedule");
+  static_assert(SPB > NR, "the first row block staged in the loop is staged at iteration >= 0");
   bf16x8 ftv[NT], ftk[NT];                    // transposed dO and Q fragments of the dV/dK pairs
   Rows rows_nx;                               // row offsets of the copy step's subtile
   // The statistics pair: S and dP of a step start as MFMAs of A = (hi, lo) of the row's -LSE/scale
@@ -295,6 +310,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     rem_apply(mp, ms, Pf, Sf, Ph, Sh, Qs, dOs);
   };
   int h3, subc;                               // head of the copy step i+3 and subtile of min(i+3, nsteps-1)
+  // row block staging: block stage_blk is staged in the iteration where to_stage reaches 0
+  int stage_blk = 1, to_stage = SPB * G - NR;
   int h0 = 0, sub0 = 0;                       // head and subtile of step i
   uint32_t hoff3, hst3;                       // its head offsets in Q/dO rows and in the statistics
   auto body = [&](f32x16& Sc, f32x16& dPc, f32x16& Sn, f32x16& dPn, const bf16x8 (&Pp)[2], const bf16x8 (&Sp)[2],
@@ -309,11 +326,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     constexpr uint32_t slot3 = (uint32_t)((p + NR - 2) % NR) * 2 * QB;
     const bool next_sub = i + NR - 1 < nsteps && h3 == G - 1;   // step i+4 starts a subtile
     const bool new_blk = next_sub && (subc + 1) % SPB == 0;      // ... and a row block
-    if (new_blk) {
-      const int blk = (subc + 1) / SPB;
-      s_row[blk & 1][tid] = pre_row;
-      s_qpos[blk & 1][tid] = pre_qpos;
-    }
+    RowIdx rows_raw;
     bf16x8 fq[KS], fo[KS], ast;
     auto load_frag = [&](int f) __attribute__((always_inline)) {   // operands of pair f
       // (the operand of the pair's second MFMA is read first: the wait for the first covers both)
@@ -406,23 +419,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         });
       }
       if constexpr (si == BAR) {
+        // (a row block staged by LDS-DMA two iterations ago is older than the last iteration's
+        // copies: this wait covers it, and the barrier makes it visible)
         wait_vmem<(NR - 4) * (CPS + 1)>();
-        if (new_blk) wait_lds<0>();   // the staged row block is written before the barrier
         barrier_only();
+      }
+      if constexpr (si == BAR + 1) {
+        if (next_sub) rows_raw = read_rows(subc + 1);
       }
       if constexpr (si >= CP0 && si < CP0 + CPD * CPS && (si - CP0) % CPD == 0) issue_one(slot3, hoff3, rows_nx, (si - CP0) / CPD);
       if constexpr (si == ST_SLOT) issue_stat(slot3, hst3, rows_nx);
       if constexpr (si == ROW_SLOT) {
         if (next_sub) {
           subc += 1;
-          rows_nx = fetch_rows(subc);
+          rows_nx = row_offsets(rows_raw);
         }
-        if (new_blk) {
-          const int nxt = ((subc / SPB) + 1) * IDX_BLK + tid;
-          if (nxt - tid < nq) {
-            pre_row = ql[min(nxt, nq - 1)];
-            pre_qpos = nxt < nq ? a.plan.row_pos[pre_row] : -1;
-          }
+        // row block stage_blk starts at step stage_blk * SPB * G, the copy step of iteration i + 3,
+        // and iteration i + 2 reads its first subtile's rows: stage it now (the copies of
+        // iteration i + 1 then lie between it and that read's wait), into the buffer of block
+        // stage_blk - 2, whose last reader was more than SPB * G - 6 steps ago
+        if (--to_stage == 0) {
+          if (stage_blk * IDX_BLK < nq) stage_block(stage_blk);
+          stage_blk += 1;
+          to_stage = SPB * G;
         }
       }
       sched_fence();

@@ -60,14 +60,14 @@ struct psattn_tree {
   int64_t Ns = 0, Nu = 0, nvis = 0;
   // plan (host copy)
   Shape shape{};
-  std::vector<int32_t> row_pos, row_slot, q_list, kv_list, pad_slots;
+  std::vector<int32_t> row_pos, row_slot, q_list, q_pos, kv_list, pad_slots;
   std::vector<FwdItem> fwd;
   std::vector<MergeEntry> merge;
   std::vector<BkvItem> bkv;
   std::vector<ReduceEntry> reduce;
   int64_t fwd_part_rows = 0, bkv_part_tiles = 0;
   // device image of the plan
-  size_t o_row_pos = 0, o_row_slot = 0, o_q = 0, o_kv = 0, o_fwd = 0, o_merge = 0, o_bkv = 0, o_reduce = 0, o_pad = 0;
+  size_t o_row_pos = 0, o_row_slot = 0, o_q = 0, o_qpos = 0, o_kv = 0, o_fwd = 0, o_merge = 0, o_bkv = 0, o_reduce = 0, o_pad = 0;
   size_t plan_bytes = 0;
   std::vector<uint8_t> image;
   void* dev = nullptr;
@@ -263,6 +263,9 @@ psattn_status check_plan(const psattn_tree* t) {
   }
   for (int64_t i = 0; i < nql; ++i)
     if (t->q_list[i] < 0 || t->q_list[i] >= ns) return bad("q_list row outside [0, Ns)", i);
+  if ((int64_t)t->q_pos.size() != nql) return bad("q_pos length", (int64_t)t->q_pos.size());
+  for (int64_t i = 0; i < nql; ++i)
+    if (t->q_pos[i] != t->row_pos[t->q_list[i]]) return bad("q_pos entry", i);
   for (int64_t i = 0; i < nkl; ++i)
     if (t->kv_list[i] < 0 || t->kv_list[i] >= slots) return bad("kv_list slot outside the pool", i);
   for (size_t i = 0; i < t->pad_slots.size(); ++i)
@@ -598,6 +601,12 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   if (t->fwd.size() > (size_t)INT32_MAX || t->bkv.size() > (size_t)INT32_MAX)
     return fail(PSATTN_E_UNSUPPORTED, "too many work items");
 
+  // sequence position of every q_list entry, so that kernels staging consumer rows need no
+  // dependent load; the device copy is preceded by -1, the position of a row past a list
+  t->q_pos.resize(t->q_list.size());
+  for (size_t i = 0; i < t->q_list.size(); ++i) t->q_pos[i] = t->row_pos[t->q_list[i]];
+  const int32_t past_list = -1;
+
   // ---------------- device image ----------------
   size_t cur = 0;
   auto place = [&](size_t bytes) {
@@ -608,6 +617,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   t->o_row_pos = place(t->row_pos.size() * 4);
   t->o_row_slot = place(t->row_slot.size() * 4);
   t->o_q = place(t->q_list.size() * 4);
+  t->o_qpos = place((t->q_pos.size() + 1) * 4);
   t->o_kv = place(t->kv_list.size() * 4);
   t->o_fwd = place(t->fwd.size() * sizeof(FwdItem));
   t->o_merge = place(t->merge.size() * sizeof(MergeEntry));
@@ -622,6 +632,8 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   put(t->o_row_pos, t->row_pos.data(), t->row_pos.size() * 4);
   put(t->o_row_slot, t->row_slot.data(), t->row_slot.size() * 4);
   put(t->o_q, t->q_list.data(), t->q_list.size() * 4);
+  put(t->o_qpos, &past_list, 4);
+  put(t->o_qpos + 4, t->q_pos.data(), t->q_pos.size() * 4);
   put(t->o_kv, t->kv_list.data(), t->kv_list.size() * 4);
   put(t->o_fwd, t->fwd.data(), t->fwd.size() * sizeof(FwdItem));
   put(t->o_merge, t->merge.data(), t->merge.size() * sizeof(MergeEntry));
@@ -637,6 +649,7 @@ PlanView plan_view(const psattn_tree* t) {
   v.row_pos = (const int32_t*)(b + t->o_row_pos);
   v.row_slot = (const int32_t*)(b + t->o_row_slot);
   v.q_list = (const int32_t*)(b + t->o_q);
+  v.q_pos = (const int32_t*)(b + t->o_qpos) + 1;
   v.kv_list = (const int32_t*)(b + t->o_kv);
   v.fwd = (const FwdItem*)(b + t->o_fwd);
   v.merge = (const MergeEntry*)(b + t->o_merge);
@@ -965,6 +978,7 @@ psattn_status psattn_tree_plan_array(const psattn_tree* t, int which, const int3
     case 6: *data = (const int32_t*)t->reduce.data(); *count = (int64_t)t->reduce.size(); *width = 8; break;
     case 7: *data = t->pad_slots.data(); *count = (int64_t)t->pad_slots.size(); *width = 1; break;
     case 8: *data = t->row_slot.data(); *count = (int64_t)t->row_slot.size(); *width = 1; break;
+    case 9: *data = t->q_pos.data(); *count = (int64_t)t->q_pos.size(); *width = 1; break;
     default: return fail(PSATTN_E_INVALID_ARG, "unknown plan array %d", which);
   }
   return PSATTN_OK;

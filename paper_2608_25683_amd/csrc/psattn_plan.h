@@ -65,6 +65,7 @@ struct PlanView {
   const int32_t* row_pos;   // [Ns] sequence position of each packed row
   const int32_t* row_slot;  // [Ns] pool slot of each packed row's K/V
   const int32_t* q_list;
+  const int32_t* q_pos;     // sequence position of each q_list entry; q_pos[-1] = -1
   const int32_t* kv_list;
   const FwdItem* fwd;
   const MergeEntry* merge;

@@ -45,7 +45,7 @@ EXPORTED = [
 KVM_EVENTS = {0: "alloc", 1: "refill", 2: "evict", 3: "free"}
 
 PLAN_ARRAYS = {"row_pos": 0, "q_list": 1, "kv_list": 2, "fwd_items": 3, "fwd_merges": 4, "bkv_items": 5,
-               "bkv_reduces": 6, "pad_slots": 7, "row_slot": 8}
+               "bkv_reduces": 6, "pad_slots": 7, "row_slot": 8, "q_pos": 9}
 
 
 class PsattnError(RuntimeError):
