@@ -329,8 +329,8 @@ psattn_status psattn_tree_get_info(const psattn_tree* tree, psattn_tree_info* in
  *   2 kv_list                 pool slots referenced by work items
  *   3 fwd_items [n][8]        q_off nq kv_off nkv kv_pos0 head0 part nfull
  *   4 fwd_merges [n][4]       q_off nq part0 nparts
- *   5 bkv_items [n][10]       kv_off nk kv_pos0 q_off nq hk part mask_lo mask_hi 0
- *   6 bkv_reduces [n][8]      kv_off nk hk part0 nparts 0 0 0
+ *   5 bkv_items [n][10]       kv_off nk kv_pos0 q_off nq hk part mask_lo mask_hi acc
+ *   6 bkv_reduces [n][8]      kv_off nk hk part0 nparts acc 0 0
  *   7 pad_slots [n]           pool slots that hold no token
  *   8 row_slot [Ns]           pool slot of each packed row's K/V
  *   9 q_pos                   sequence position of each q_list entry

@@ -6,11 +6,11 @@
 // every descendant node, i.e. all branches reusing the prefix.  For each 32-row subtile and each
 // query head of the group it computes S = Q K^T and dP = dO V^T (lane <-> key),
 // P = exp(S*scale - LSE), dS = P*(dP - Delta), then dV += P^T dO and dK += dS^T Q, whose B
-// operands (dO^T, Q^T) come from transposing LDS reads of the row-major tiles.  The main form
+// operands (dO^T, Q^T) come from transposing LDS reads of the row-major tiles.  The kernel
 // (bwd_kv_bf16_1w_kernel) runs one wavefront per SIMD, wave w keeping keys 32w..32w+31 of K and
 // V and their dK/dV accumulators in registers, and streams Q/dO rows and the LSE/Delta values
-// global -> LDS directly into a five-step ring.  Consumer-row indices are staged in LDS 256 at a
-// time.
+// global -> LDS directly into a five-step ring.  Consumer-row indices and positions are staged
+// in LDS 256 at a time, each block copied there (LDS-DMA) two iterations before it is read.
 //
 // bf16 dQ kernel: the same items as the forward kernel and its structure (NH 32-row halves per
 // wave); recomputes S^T and dP^T per key tile and accumulates dQ^T += K^T dS^T, K^T again from

@@ -404,7 +404,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
   // (free once every wave has finished the PV products above; padded row stride OS), then copies
   // them out 16 bytes per lane, 1 KB of consecutive row bytes per instruction.  Row index and
   // validity of staged row r come from lane r % 32 of the half that owns it.  With O_lo, a second
-  // round stages and writes the rounding residuals O - bf16(O) the same way.
+  // pass stages and writes the rounding residuals O - bf16(O) the same way.
   constexpr int OS = RB + 16;
   static_assert(NW * 32 * NH * OS <= NS * 2 * TB, "staged O rows fit the ring");
   const bool direct = it.part < 0;
@@ -434,7 +434,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
     }
   }
   if (direct) {
-    // round 0: bf16(O) into O; round 1: bf16(O - bf16(O)) into O_lo
+    // first pass: bf16(O) into O; second pass: bf16(O - bf16(O)) into O_lo
     auto write_rows = [&](bool lo, uint8_t* dst) __attribute__((always_inline)) {
 #pragma unroll
       for (int rh = 0; rh < NH; ++rh) {
