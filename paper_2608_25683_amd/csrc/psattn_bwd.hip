@@ -136,6 +136,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     uint32_t st;         // 4 * row lane/2 (+ the distance from the -LSE/scale to the -Delta array on odd lanes)
   };
   const uint32_t nd_dist = (uint32_t)((const char*)a.kv_nd - (const char*)a.kv_nls);
+  const uint32_t stat_row = (uint32_t)hq * 4;   // bytes per row of the [Ns][Hq] statistics
   const uint32_t row_bytes = (uint32_t)hq * RB;
   // rows of subtile sub (staged): the LDS reads, then the offsets (split, so that the reads can be
   // issued well before their results are needed)
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int r = ((wave + 4 * j) % NI) * RPI + crow;
       o.off[j] = (uint32_t)x.r[j] * row_bytes + ((cpc ^ swz<D>(r)) << 4);
     }
-    o.st = (uint32_t)x.r[CPS] * 4 + ((lane & 1) ? nd_dist : 0u);
+    o.st = (uint32_t)x.r[CPS] * stat_row + ((lane & 1) ? nd_dist : 0u);
     return o;
   };
   auto fetch_rows = [&](int sub) __attribute__((always_inline)) { return row_offsets(read_rows(sub)); };
@@ -169,7 +170,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     gsrc[j] = tens ? a.dO : a.Q;
     gdst[j] = (uint32_t)(tens * QB + ins * 1024);
   }
-  const uint32_t hoff0 = (uint32_t)(hk * G) * RB, hst0 = (uint32_t)(hk * G) * (uint32_t)ns * 4;
+  const uint32_t hoff0 = (uint32_t)(hk * G) * RB, hst0 = (uint32_t)(hk * G) * 4;
   // copy j of a step (head offsets hoff/hst, ring slot byte offset slot_off) into its ring slot
   auto issue_one = [&](uint32_t slot_off, uint32_t hoff, const Rows& rw, int j) __attribute__((always_inline)) {
     copy16_to_lds_off(gsrc[j], rw.off[j] + hoff, smem_base + slot_off + gdst[j]);
@@ -458,7 +459,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const bool wrap = h3 == G - 1;
       h3 = wrap ? 0 : h3 + 1;
       hoff3 = wrap ? hoff0 : hoff3 + RB;
-      hst3 = wrap ? hst0 : hst3 + (uint32_t)ns * 4;
+      hst3 = wrap ? hst0 : hst3 + 4;
     }
   };
 
@@ -472,14 +473,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const Rows rw = fetch_rows(sc / G);
 #pragma unroll
     for (int j = 0; j < CPS; ++j) issue_one(p * 2 * QB, hoff0 + h * RB, rw, j);
-    issue_stat(p * 2 * QB, hst0 + (uint32_t)h * ns * 4, rw);
+    issue_stat(p * 2 * QB, hst0 + (uint32_t)h * 4, rw);
   }
   {
     const int sc = min(NR - 2, nsteps - 1);
     h3 = sc % G;
     subc = sc / G;
     hoff3 = hoff0 + h3 * RB;
-    hst3 = hst0 + (uint32_t)h3 * ns * 4;
+    hst3 = hst0 + (uint32_t)h3 * 4;
     rows_nx = fetch_rows(subc);
   }
   wait_vmem<(NR - 3) * (CPS + 1)>();
@@ -671,8 +672,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
     row_ok[rh] = ridx[rh] < it.nq;
     row[rh] = a.plan.q_list[it.q_off + (row_ok[rh] ? ridx[rh] : it.nq - 1)];
     lim[rh] = min(nkv - 1, a.plan.row_pos[row[rh]] - it.kv_pos0);
-    lse2[rh] = a.lse2[(size_t)head * a.s.ns + row[rh]];
-    del[rh] = a.delta[(size_t)head * a.s.ns + row[rh]];
+    lse2[rh] = a.lse2[(size_t)row[rh] * a.s.hq + head];
+    del[rh] = a.delta[(size_t)row[rh] * a.s.hq + head];
     const size_t o = ((size_t)row[rh] * a.s.hq + head) * D + 8 * hh;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
@@ -950,7 +951,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3 - NH,
       if (it.part < 0) {
         const uint32_t w = split_bf16(-del[rh]);
         const float d0 = bf2f(w & 0xffffu) + bf2f(w >> 16);   // the -Delta the dP products started from
-        ((uint32_t*)a.kv_nd)[(size_t)head * a.s.ns + row[rh]] = split_bf16(d0 - e);
+        ((uint32_t*)a.kv_nd)[(size_t)row[rh] * a.s.hq + head] = split_bf16(d0 - e);
       } else {
         a.part_eps[((size_t)it.part + ridx[rh]) * a.s.hq + head] = e;
       }
@@ -1055,7 +1056,7 @@ __global__ __launch_bounds__(256) void bwd_kv_f32_kernel(BwdArgs a) {
         const int r = Q_SUB * sub + tid;
         const int row = ql[min(r, it.nq - 1)];
         s_lse[tid] = a.LSE[(size_t)head * a.s.ns + row];
-        s_del[tid] = a.delta[(size_t)head * a.s.ns + row];
+        s_del[tid] = a.delta[(size_t)row * a.s.hq + head];
         s_qpos[tid] = r < it.nq ? a.plan.row_pos[row] : -1;
       }
       __syncthreads();
@@ -1114,7 +1115,7 @@ __global__ __launch_bounds__(512) void bwd_dq_f32_kernel(BwdArgs a) {
   const int row = a.plan.q_list[it.q_off + (row_ok ? ridx : it.nq - 1)];
   const int qpos = a.plan.row_pos[row];
   const float lse = a.LSE[(size_t)head * a.s.ns + row];
-  const float del = a.delta[(size_t)head * a.s.ns + row];
+  const float del = a.delta[(size_t)row * a.s.hq + head];
   float q[H], dov[H], dq[H];
   {
     const size_t o = ((size_t)row * a.s.hq + head) * D + half * H;
@@ -1225,12 +1226,11 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
     const int64_t pr = pair0 + p * per_pass;
     if (pr < npairs && sub == 0) {
       const int row = (int)(pr / hq), h = (int)(pr % hq);
-      const size_t o = (size_t)h * ns + row;
-      const float lse = a.LSE[o];
-      a.delta[o] = acc[p];
-      a.lse2[o] = lse * kLog2e;
-      ((uint32_t*)a.kv_nls)[o] = split_bf16(-lse / a.s.scale);
-      ((uint32_t*)a.kv_nd)[o] = split_bf16(-acc[p]);
+      const float lse = a.LSE[(size_t)h * ns + row];
+      a.delta[pr] = acc[p];   // the statistics are [Ns][Hq]: pair pr's entry, written in order
+      a.lse2[pr] = lse * kLog2e;
+      ((uint32_t*)a.kv_nls)[pr] = split_bf16(-lse / a.s.scale);
+      ((uint32_t*)a.kv_nd)[pr] = split_bf16(-acc[p]);
     }
   }
 }
@@ -1270,7 +1270,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_dq_kernel(BwdArgs a) {
       const int i = idx / hq, h = idx % hq;
       float s = 0.f;
       for (int j = 0; j < e.nparts; ++j) s += a.part_eps[((size_t)e.part0 + (size_t)j * bmq + i) * hq + h];
-      uint32_t* nd = (uint32_t*)a.kv_nd + (size_t)h * a.s.ns + a.plan.q_list[e.q_off + i];
+      uint32_t* nd = (uint32_t*)a.kv_nd + (size_t)a.plan.q_list[e.q_off + i] * hq + h;
       const uint32_t w = *nd;
       *nd = split_bf16(bf2f(w & 0xffffu) + bf2f(w >> 16) - s);
     }

@@ -35,10 +35,10 @@ struct BwdArgs {
   float* dQ;
   float* dK;
   float* dV;
-  float* delta;    // [Hq][Ns]
-  float* lse2;     // [Hq][Ns] LSE * log2(e)
-  float* kv_nls;   // [Hq][Ns] -LSE / scale   (start of the dK/dV kernels' S accumulators)
-  float* kv_nd;    // [Hq][Ns] -Delta         (start of their dP accumulators; bf16: the exact
+  float* delta;    // [Ns][Hq]
+  float* lse2;     // [Ns][Hq] LSE * log2(e)
+  float* kv_nls;   // [Ns][Hq] -LSE / scale   (start of the dK/dV kernels' S accumulators)
+  float* kv_nd;    // [Ns][Hq] -Delta         (start of their dP accumulators; bf16: the exact
                    //                          Delta' from the dQ pass, which runs first)
   float* part_dq;  // [partial rows][Hq][d]
   float* part_eps; // [partial rows][Hq] row sums of dS' of each piece (bf16)
