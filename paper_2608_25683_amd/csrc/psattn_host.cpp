@@ -487,8 +487,13 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
       int64_t full_by_mask = (int64_t)f.min_qpos + 1 - f.kv_pos0;
       full_by_mask = full_by_mask < 0 ? 0 : full_by_mask / KV_TILE;
       int32_t nfull = (int32_t)std::min(full_by_len, full_by_mask);
-      for (int c2 = 0; c2 < n_chunks; ++c2)
-        t->fwd.push_back({f.q_off, f.nq, f.kv_off, f.nkv, f.kv_pos0, c2 * s.hc, f.part, nfull});
+      // the task's head chunks with the kv head varying fastest: consecutive workgroups, which the
+      // dispatcher deals round-robin to the 8 XCDs, then read one kv head per XCD (each XCD's L2
+      // holds one kv head's K/V) whatever the number of query heads per kv head
+      for (int j = 0; j < n_chunks; ++j) {
+        const int kvh = j % t->hkv, sub = j / t->hkv;
+        t->fwd.push_back({f.q_off, f.nq, f.kv_off, f.nkv, f.kv_pos0, kvh * s.g + sub * s.hc, f.part, nfull});
+      }
     }
   }
 
