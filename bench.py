@@ -22,8 +22,10 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 matrix
 PEAK_HBM_GBS = 8000.0
 METRIC = "effective fwd+bwd attention tokens/sec (unshared-equiv) + % bf16 MFMA peak"
+# sources a committed traffic summary depends on: the kernels, and the planner that orders and
+# shapes their work items (a summary whose hash no longer matches is not used)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_25683_amd", "csrc", f) for f in
-               ("psattn_device.h", "psattn_fwd.hip", "psattn_bwd.hip")]
+               ("psattn_device.h", "psattn_fwd.hip", "psattn_bwd.hip", "psattn_plan.h", "psattn_host.cpp")]
 
 # algorithmic matmul flops of each kernel per visible (query, key) pair and query head, per unit
 # of head_dim, in the FlashAttention convention that F_alg = 14 d per pair follows: forward S and
