@@ -535,11 +535,16 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
     int64_t per_cu = total_b * t->hkv / std::max(1, 2 * num_cus);
     chunk_rows = std::max<int64_t>(2048, per_cu / BKV_TILE / Q_SUB * Q_SUB);
   }
-  struct BTask { int32_t kv_off, nk, kv_pos0, q_off, nq, mask_lo, mask_hi, part_base, nparts, chunk, acc; double cost; };
+  struct BTask {
+    int32_t kv_off, nk, kv_pos0, q_off, nq, mask_lo, mask_hi, part_base, nparts, chunk, acc;
+    double cost, key;
+    int64_t group;   // first task of the node's tasks on the same chunk
+  };
   std::vector<BTask> btasks;
   std::vector<ReduceEntry> reduces;
   int64_t part_tiles = 0;
   for (int m = 0; m < N; ++m) {
+    const size_t first_task = btasks.size();
     for (int b0 = 0; b0 < t->seg_len[m]; b0 += BKV_TILE) {
       int nk = std::min(BKV_TILE, t->seg_len[m] - b0);
       // an external node's tiles add this call's consumers to the gradients that earlier calls
@@ -576,15 +581,45 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
         btasks.push_back(b);
       }
     }
+    // sort key: the largest cost among the node's tasks on the same chunk of consumer rows.  A
+    // tile sees 128 fewer of the node's own rows than the one before it, so the tiles' own costs
+    // differ; under one key they stay together through the longest-first sort, run at the same
+    // time and stream that chunk's rows through L2 once
+    std::vector<double> chunk_max;
+    std::vector<int64_t> chunk_first;
+    for (size_t i = first_task; i < btasks.size(); ++i) {
+      const size_t j = (size_t)btasks[i].chunk;
+      if (chunk_max.size() <= j) {
+        chunk_max.resize(j + 1, 0.0);
+        chunk_first.resize(j + 1, -1);
+      }
+      chunk_max[j] = std::max(chunk_max[j], btasks[i].cost);
+      if (chunk_first[j] < 0) chunk_first[j] = (int64_t)i;
+    }
+    for (size_t i = first_task; i < btasks.size(); ++i) {
+      if (btasks[i].nparts == 1 && desc_len[m] > 0) {
+        btasks[i].key = chunk_max[0];
+        btasks[i].group = chunk_first[0];
+      } else {   // (tiles split into chunks keep their own cost: equal chunks already sort together)
+        btasks[i].key = btasks[i].cost;
+        btasks[i].group = (int64_t)i;
+      }
+    }
   }
   if (part_tiles > INT32_MAX / 2) return fail(PSATTN_E_UNSUPPORTED, "too many partial tiles");
   t->bkv_part_tiles = part_tiles;
   t->reduce = reduces;
   {
-    std::vector<double> c(btasks.size());
-    for (size_t i = 0; i < btasks.size(); ++i) c[i] = btasks[i].cost;
+    // longest first by key; a group (equal keys can be several groups) stays one run, its tiles
+    // in order
+    std::vector<int> ord(btasks.size());
+    std::iota(ord.begin(), ord.end(), 0);
+    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) {
+      if (btasks[x].key != btasks[y].key) return btasks[x].key > btasks[y].key;
+      return btasks[x].group < btasks[y].group;
+    });
     t->bkv.clear();
-    for (int i : longest_first(c)) {
+    for (int i : ord) {
       const BTask& b = btasks[i];
       for (int hk = 0; hk < t->hkv; ++hk) {
         int32_t part = b.nparts > 1 ? b.part_base + hk * b.nparts + b.chunk : -1;

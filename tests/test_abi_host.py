@@ -335,6 +335,24 @@ def test_items_are_longest_first():
     fwd = t.plan_array("fwd_items")
     cost = fwd[:, 1].astype(np.int64) * fwd[:, 3]
     assert np.all(np.diff(cost) <= 0)
+    # dK/dV items: longest first by a key that is the item's own cost, except for a node with
+    # descendants whose tiles each take one chunk of consumer rows: its tiles stream the same rows
+    # (its descendants' first), so they share the largest of their costs as key and form one run
+    # that runs together and streams those rows through L2 once
     bkv = t.plan_array("bkv_items")
     cost = bkv[:, 1].astype(np.int64) * bkv[:, 4]
-    assert np.all(np.diff(cost) <= 0)
+    tr = wl.tree
+    slot_row = {int(sl): r for r, sl in enumerate(tr.row_slots())}
+    row_node = np.repeat(np.arange(tr.num_nodes), tr.seg_len)[np.argsort(np.repeat(tr.row_off, tr.seg_len) + np.concatenate([np.arange(L) for L in tr.seg_len]))]
+    kvl = t.plan_array("kv_list")
+    node = np.array([row_node[slot_row[int(kvl[o])]] for o in bkv[:, 0]])
+    has_desc = np.zeros(tr.num_nodes, bool)
+    has_desc[[p for p in tr.parent if p >= 0]] = True
+    grouped = (bkv[:, 6] == -1) & has_desc[node]
+    key = cost.copy()
+    for n in np.unique(node[grouped]):
+        sel = grouped & (node == n)
+        key[sel] = cost[sel].max()
+        run = np.flatnonzero(sel)
+        assert run[-1] - run[0] + 1 == len(run), f"the tiles of node {n} are not one run"
+    assert np.all(np.diff(key) <= 0)
