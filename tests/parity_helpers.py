@@ -90,8 +90,11 @@ def check_full(wl, gpu, ref):
 # root is read by every row), the first and the last tile of one leaf, and -- from the same
 # per-row forward -- O and LSE of every row that consumes the most-shared node, for every query
 # head.  dQ is checked on every row of the first and the last query tile of the most-shared node
-# and of the leaf.  The kv heads run in parallel worker processes (numpy only; the inputs and the
-# GPU outputs are shared through memory-mapped files).
+# and of the leaf.  Two complete slices are evaluated besides and gated on their own: dK and dV
+# of every key of the most-shared node and of the leaf on kv head 0 (the c2 root's 4096 keys,
+# each summed over all its consumers through partial tiles and the chunk reduction), and dQ of
+# every row of one branch (a leaf of at most 1024 rows) for the query heads of kv head 0.  The kv heads run in parallel worker
+# processes (numpy only; the inputs and the GPU outputs are shared through memory-mapped files).
 
 def _most_shared_and_leaf(t):
     ti = O.TreeIndex(t.parent, t.seg_len, t.row_off)
@@ -116,6 +119,12 @@ def _stats(g, r):
 
 def _full_size_worker(job):
     """One kv head: oracle values of the selected outputs, compared with the GPU's (partial stats)."""
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=job["threads"]):
+        return _full_size_job(job)
+
+
+def _full_size_job(job):
     import numpy as _np
     d = {k: _np.load(v, mmap_mode="r") for k, v in job["files"].items()}
     ti = O.TreeIndex(d["parent"], d["seg_len"], d["row_off"])
@@ -126,6 +135,8 @@ def _full_size_worker(job):
     slots = d["row_slots"][job["keys"]]
     out = {"dK": _stats(_np.asarray(d["gdK"][slots, g], _np.float64), dk),
            "dV": _stats(_np.asarray(d["gdV"][slots, g], _np.float64), dv)}
+    if job["complete"]:   # job["keys"] is then the complete slice
+        out["dK complete"], out["dV complete"] = out["dK"], out["dV"]
     o_st, l_st, rs = [], [], 0.0
     for m, (cons, Oc, LSEc) in fo.items():
         o_st.append(_stats(_np.asarray(d["gO"][cons][:, heads], _np.float64), Oc))
@@ -137,14 +148,19 @@ def _full_size_worker(job):
     out["rowsum"] = rs
     out["rows_o"] = int(sum(len(c) for c, _, _ in fo.values()))
     dq = O.rows_dq(ti, d["Q"], d["K"], d["V"], d["dO"], scale, job["dq_rows"], heads)
-    out["dQ"] = _stats(_np.asarray(d["gdQ"][job["dq_rows"]][:, heads], _np.float64), dq)
+    gq = _np.asarray(d["gdQ"][job["dq_rows"]][:, heads], _np.float64)
+    out["dQ"] = _stats(gq, dq)
+    if job["complete"]:
+        sel = _np.isin(_np.asarray(job["dq_rows"]), _np.asarray(job["leaf_rows"]))
+        out["dQ complete"] = _stats(gq[sel], dq[sel])
     return out
 
 
-def check_full_size(wl, gpu, workers=8, tmpdir=None, gate=("O", "LSE", "dQ", "dK", "dV")):
+def check_full_size(wl, gpu, workers=8, tmpdir=None, gate=("O", "LSE", "dQ", "dK", "dV"), complete=True):
     """Element-by-element parity of the selected outputs of a full-size workload (see above);
     returns {tensor: (max-abs, rel-L2)} plus the counts checked.  Only the tensors in ``gate``
-    must meet the tolerances; the others are reported."""
+    (and their complete slices, when ``complete``) must meet the tolerances; the others are
+    reported."""
     import multiprocessing as mp
     import shutil
     import tempfile
@@ -157,6 +173,14 @@ def check_full_size(wl, gpu, workers=8, tmpdir=None, gate=("O", "LSE", "dQ", "dK
     dq_rows = _tiles(int(t.row_off[shared]), int(t.seg_len[shared]), 64)
     if leaf != shared:
         dq_rows = sorted(set(dq_rows) | set(_tiles(int(t.row_off[leaf]), int(t.seg_len[leaf]), 64)))
+    node_rows = lambda n: list(range(int(t.row_off[n]), int(t.row_off[n]) + int(t.seg_len[n])))
+    keys_all = sorted(set(node_rows(shared)) | set(node_rows(leaf)))
+    # the branch whose every dQ row is checked: the longest leaf of at most 1024 rows (else the
+    # shortest), so that the per-row oracle stays within seconds
+    leaves = [n for n in range(t.num_nodes) if not ti.children[n]]
+    short = [n for n in leaves if int(t.seg_len[n]) <= 1024]
+    branch = max(short, key=lambda n: (int(t.seg_len[n]), n)) if short else min(leaves, key=lambda n: (int(t.seg_len[n]), n))
+    leaf_rows = node_rows(branch)
     tmp = tempfile.mkdtemp(prefix="psattn_parity_", dir=tmpdir)
     try:
         arrays = {"parent": t.parent, "seg_len": t.seg_len, "row_off": t.row_off, "row_slots": t.row_slots(),
@@ -168,13 +192,17 @@ def check_full_size(wl, gpu, workers=8, tmpdir=None, gate=("O", "LSE", "dQ", "dK
             files[k] = f"{tmp}/{k}.npy"
             np.save(files[k], np.ascontiguousarray(v))
         G = wl.hq // wl.hkv
-        jobs = [{"files": files, "g": g, "G": G, "scale": wl.scale, "keys": keys, "dq_rows": dq_rows}
-                for g in range(wl.hkv)]
-        threads = max(1, (len(os.sched_getaffinity(0)) // max(1, min(workers, wl.hkv))))
+        cores = len(os.sched_getaffinity(0))
+        threads = max(1, cores // max(1, min(workers, wl.hkv)))
+        jobs = [{"files": files, "g": g, "G": G, "scale": wl.scale, "keys": keys, "dq_rows": dq_rows,
+                 "complete": False, "threads": threads} for g in range(wl.hkv)]
+        if complete:   # the long job of the pool: more threads
+            jobs[0].update(complete=True, keys=keys_all, dq_rows=sorted(set(dq_rows) | set(leaf_rows)),
+                           leaf_rows=leaf_rows, threads=max(threads, cores // 2))
         env_keys = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
         saved = {k: os.environ.get(k) for k in env_keys}
         for k in env_keys:
-            os.environ[k] = str(threads)
+            os.environ[k] = str(max(j["threads"] for j in jobs))
         try:
             with mp.get_context("spawn").Pool(min(workers, wl.hkv)) as pool:
                 parts = pool.map(_full_size_worker, jobs)
@@ -189,14 +217,18 @@ def check_full_size(wl, gpu, workers=8, tmpdir=None, gate=("O", "LSE", "dQ", "dK
     tau_abs, tau_rel = TOL[wl.dtype]
     res = {"keys": len(keys), "dq_rows": len(dq_rows), "o_rows": parts[0]["rows_o"], "shared_node": shared,
            "leaf": leaf}
-    for name in ("O", "LSE", "dQ", "dK", "dV"):
-        mx = max(p[name][0] for p in parts)
-        num = sum(p[name][1] for p in parts)
-        den = sum(p[name][2] for p in parts)
+    if complete:
+        res.update({"keys complete": len(keys_all), "dq_rows complete": len(leaf_rows), "branch": branch})
+    names = ["O", "LSE", "dQ", "dK", "dV"] + (["dQ complete", "dK complete", "dV complete"] if complete else [])
+    for name in names:
+        ps = [p[name] for p in parts if name in p]
+        mx = max(x[0] for x in ps)
+        num = sum(x[1] for x in ps)
+        den = sum(x[2] for x in ps)
         rel = float(np.sqrt(num / den)) if den > 0 else float(np.sqrt(num))
         res[name] = (mx, rel)
     res["rowsum"] = max(p["rowsum"] for p in parts)
-    for name in gate:
+    for name in [n for n in names if n.split()[0] in gate]:
         mx, rel = res[name]
         assert mx <= tau_abs and rel <= tau_rel, f"{name}: max-abs {mx:.3g} (<= {tau_abs}), rel-L2 {rel:.3g} (<= {tau_rel})"
     assert res["rowsum"] <= ROWSUM_TOL[wl.dtype], f"softmax rows with the GPU LSE sum to 1 +- {res['rowsum']:.3g}"
