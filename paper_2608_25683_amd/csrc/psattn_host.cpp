@@ -538,7 +538,7 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   struct BTask {
     int32_t kv_off, nk, kv_pos0, q_off, nq, mask_lo, mask_hi, part_base, nparts, chunk, acc;
     double cost, key;
-    int64_t group;   // first task of the node's tasks on the same chunk
+    int64_t group;   // tasks of one group (same key and group) are emitted as one run
   };
   std::vector<BTask> btasks;
   std::vector<ReduceEntry> reduces;
@@ -581,29 +581,24 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
         btasks.push_back(b);
       }
     }
-    // sort key: the largest cost among the node's tasks on the same chunk of consumer rows.  A
-    // tile sees 128 fewer of the node's own rows than the one before it, so the tiles' own costs
-    // differ; under one key they stay together through the longest-first sort, run at the same
-    // time and stream that chunk's rows through L2 once
-    std::vector<double> chunk_max;
-    std::vector<int64_t> chunk_first;
-    for (size_t i = first_task; i < btasks.size(); ++i) {
-      const size_t j = (size_t)btasks[i].chunk;
-      if (chunk_max.size() <= j) {
-        chunk_max.resize(j + 1, 0.0);
-        chunk_first.resize(j + 1, -1);
+    // sort key.  The tiles of a node with descendants that each take one chunk stream the same
+    // consumer rows, the descendants' rows first.  They share the largest of their costs as key,
+    // so that they stay one run through the longest-first sort, run at the same time and stream
+    // those rows through L2 once (each tile sees 128 fewer of the node's own rows than the one
+    // before it, so their own costs differ).  Every other task keeps its own cost: a leaf's tiles
+    // share no rows beyond its own, and the chunks of a split tile are equal already.
+    double node_key = 0.0;
+    int64_t node_group = -1;
+    auto grouped = [&](const BTask& b) { return b.nparts == 1 && desc_len[m] > 0; };
+    for (size_t i = first_task; i < btasks.size(); ++i)
+      if (grouped(btasks[i])) {
+        node_key = std::max(node_key, btasks[i].cost);
+        if (node_group < 0) node_group = (int64_t)i;
       }
-      chunk_max[j] = std::max(chunk_max[j], btasks[i].cost);
-      if (chunk_first[j] < 0) chunk_first[j] = (int64_t)i;
-    }
     for (size_t i = first_task; i < btasks.size(); ++i) {
-      if (btasks[i].nparts == 1 && desc_len[m] > 0) {
-        btasks[i].key = chunk_max[0];
-        btasks[i].group = chunk_first[0];
-      } else {   // (tiles split into chunks keep their own cost: equal chunks already sort together)
-        btasks[i].key = btasks[i].cost;
-        btasks[i].group = (int64_t)i;
-      }
+      const bool g = grouped(btasks[i]);
+      btasks[i].key = g ? node_key : btasks[i].cost;
+      btasks[i].group = g ? node_group : (int64_t)i;
     }
   }
   if (part_tiles > INT32_MAX / 2) return fail(PSATTN_E_UNSUPPORTED, "too many partial tiles");
