@@ -95,6 +95,15 @@ def test_invalid_descriptors(base, mutate, status):
     assert e.value.name == status, str(e.value)
 
 
+def test_empty_tree_is_rejected():
+    # a forest with no nodes has no rows to attend: the descriptor is refused, not planned
+    z = np.zeros(0, np.int32)
+    with pytest.raises(P.PsattnError) as e:
+        _make(parent=z, seg_len=z, row_off=z, blk_ptr=np.zeros(1, np.int32), blk_base=z, blk_cap=z, blk_len=z,
+              blk_pos=z, pool_slots=16, sample_end=z, hq=4, hkv=2, head_dim=128, softmax_scale=0.1, dtype="bf16")
+    assert e.value.name == "PSATTN_E_INVALID_ARG"
+
+
 def test_size_limits_hold_only_for_bf16(base):
     # the fp32 kernels use 64-bit offsets: the same large pool is accepted there
     base.update(pool_slots=(1 << 24) + 1, dtype="fp32")
