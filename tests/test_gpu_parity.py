@@ -166,6 +166,43 @@ def test_pool_order_and_padding_do_not_change_results():
             assert np.array_equal(r1[i][w1.tree.row_slots()], r[i][w.tree.row_slots()])
 
 
+# --------------------------------------------------------------------------- the largest pool
+
+# A bf16 tree may use a pool of up to 2^24 slots and 4 GiB per K or V pool.  Here the pool has
+# exactly 2^24 slots (Hkv = 1, d = 64: 2 GiB per pool) and the tree's blocks are its last slots, so
+# every slot index and K/V byte offset the kernels form lies at the top of its range; the fp32
+# gradient pools span 4 GiB each.  Slots below the tree's are never read or written.
+def test_blocks_at_the_top_of_the_largest_pool():
+    import torch
+    from paper_2608_25683_amd import psattn as P
+    wl = W.custom([-1, 0, 0, 1], [300, 140, 90, 60], [3, 2], hq=4, hkv=1, d=64, dtype="bf16", seed=11,
+                  block_policy=lambda L: W.blocks_fixed(L, 32))
+    t = wl.tree
+    top = 1 << 24
+    shift = top - t.pool_slots
+    _say(f"largest pool: {top} slots, the tree's {t.pool_slots} at the top")
+    tree = P.Tree(t.parent, t.seg_len, t.row_off, t.blk_ptr, t.blk_base + shift, t.blk_cap, t.blk_len, t.blk_pos,
+                  top, t.sample_end, wl.hq, wl.hkv, wl.d, wl.scale, dtype="bf16", device="cuda")
+    dev = torch.device("cuda")
+    bf = torch.bfloat16
+    K = torch.empty((top, wl.hkv, wl.d), dtype=bf, device=dev)
+    V = torch.empty_like(K)
+    K[shift:] = torch.from_numpy(wl.K_pool).to(dev).to(bf)
+    V[shift:] = torch.from_numpy(wl.V_pool).to(dev).to(bf)
+    Q = torch.from_numpy(wl.Q).to(dev).to(bf)
+    dO = torch.from_numpy(wl.dO).to(dev).to(bf)
+    O_lo = torch.empty_like(Q)
+    dK = torch.empty((top, wl.hkv, wl.d), dtype=torch.float32, device=dev)
+    dV = torch.empty_like(dK)
+    Og, LSEg = P.psattn_fwd(tree, Q, K, V, O_lo=O_lo)
+    dQ, dK, dV = P.psattn_bwd(tree, Q, K, V, Og, LSEg, dO, dK=dK, dV=dV, O_lo=O_lo)
+    torch.cuda.synchronize()
+    f64 = lambda x: x.float().cpu().numpy().astype(np.float64)
+    gpu = (f64(Og), f64(LSEg), f64(dQ), f64(dK[shift:]), f64(dV[shift:]))
+    res = H.check_full(wl, gpu, H.run_oracle(wl))
+    _say(f"largest pool {res}")
+
+
 # --------------------------------------------------------------------------- full-size workloads
 
 # every kv head: all keys of the first and last 128-key tiles of the most-shared node and of a
