@@ -203,6 +203,41 @@ def test_blocks_at_the_top_of_the_largest_pool():
     _say(f"largest pool {res}")
 
 
+# The largest row range of a bf16 tree: Ns * Hq just under 2^24 (the dK/dV kernel forms 32-bit byte
+# offsets into Q and dO; Q, O and dO are 4 GiB each here, dQ 8 GiB).  65535 independent 64-token
+# roots, inputs drawn on the GPU; the oracle checks the first, a middle and the last root, whose
+# rows sit at the bottom, middle and top of the range.
+def test_rows_at_the_top_of_the_largest_row_range():
+    import torch
+    from paper_2608_25683_amd import psattn as P
+    n, L, hq, hkv, d = (1 << 16) - 1, 64, 4, 2, 128
+    wl = W.custom([-1] * n, [L] * n, list(range(n)), hq=hq, hkv=hkv, d=d, dtype="bf16", tensors=False,
+                  block_policy=lambda x: W.blocks_fixed(x, L), shuffle_pool=False)
+    t = wl.tree
+    assert t.num_rows * hq < (1 << 24) and np.array_equal(t.row_slots(), np.arange(t.num_rows))
+    _say(f"largest row range: Ns {t.num_rows}, Ns*Hq {t.num_rows * hq}")
+    tree = P.Tree.from_workload(wl, device="cuda")
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev).manual_seed(17)
+    draw = lambda shape, sd: (sd * torch.randn(shape, generator=g, device=dev)).to(torch.bfloat16)
+    Q, dO = draw((t.num_rows, hq, d), 0.5), draw((t.num_rows, hq, d), 1.0)
+    K, V = draw((t.num_rows, hkv, d), 0.5), draw((t.num_rows, hkv, d), 0.5)   # pool slot = row
+    O_lo = torch.empty_like(Q)
+    Og, LSEg = P.psattn_fwd(tree, Q, K, V, O_lo=O_lo)
+    dQ, dK, dV = P.psattn_bwd(tree, Q, K, V, Og, LSEg, dO, O_lo=O_lo)
+    torch.cuda.synchronize()
+    f64 = lambda x: x.float().cpu().numpy().astype(np.float64)
+    for root in (0, n // 2, n - 1):
+        rows = slice(root * L, (root + 1) * L)
+        one = W.custom([-1], [L], [0], hq=hq, hkv=hkv, d=d, dtype="bf16", tensors=False,
+                       block_policy=lambda x: W.blocks_fixed(x, L), shuffle_pool=False)
+        one.Q, one.dO, one.K, one.V = f64(Q[rows]), f64(dO[rows]), f64(K[rows]), f64(V[rows])
+        one.K_pool, one.V_pool = one.K, one.V
+        gpu = (f64(Og[rows]), f64(LSEg[:, rows]), f64(dQ[rows]), f64(dK[rows]), f64(dV[rows]))
+        res = H.check_full(one, gpu, H.run_oracle(one))
+        _say(f"root {root} (rows {rows.start}..{rows.stop - 1}): {res}")
+
+
 # --------------------------------------------------------------------------- full-size workloads
 
 # every kv head: all keys of the first and last 128-key tiles of the most-shared node and of a
