@@ -532,7 +532,9 @@ psattn_status build_plan(psattn_tree* t, const psattn_plan_opts& o) {
   } else if (o.bwd_q_chunk < 0) {
     chunk_rows = INT64_MAX;
   } else {
-    int64_t per_cu = total_b * t->hkv / std::max(1, 2 * num_cus);
+    // a chunk holds at most one CU's share of the dK/dV work: a tile whose consumers fit in one
+    // share runs as one item, with no partial tiles to write and sum
+    int64_t per_cu = total_b * t->hkv / std::max(1, num_cus);
     chunk_rows = std::max<int64_t>(2048, per_cu / BKV_TILE / Q_SUB * Q_SUB);
   }
   struct BTask {
