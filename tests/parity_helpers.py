@@ -92,9 +92,10 @@ def check_full(wl, gpu, ref):
 # head.  dQ is checked on every row of the first and the last query tile of the most-shared node
 # and of the leaf.  Two complete slices are evaluated besides and gated on their own: dK and dV
 # of every key of the most-shared node and of the leaf on kv head 0 (the c2 root's 4096 keys,
-# each summed over all its consumers through partial tiles and the chunk reduction), and dQ of
-# every row of one branch (a leaf of at most 1024 rows) for the query heads of kv head 0.  The kv heads run in parallel worker
-# processes (numpy only; the inputs and the GPU outputs are shared through memory-mapped files).
+# each summed over all its consumers; on c4 and c2-small through partial tiles and the chunk
+# sum), and dQ of every row of one branch (a leaf of at most 1024 rows) for the query heads of kv
+# head 0.  The kv heads run in parallel worker processes (numpy only; the inputs and the GPU
+# outputs are shared through memory-mapped files).
 
 def _most_shared_and_leaf(t):
     ti = O.TreeIndex(t.parent, t.seg_len, t.row_off)
