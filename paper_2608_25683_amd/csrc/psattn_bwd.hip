@@ -1164,13 +1164,14 @@ __global__ __launch_bounds__(512) void bwd_dq_f32_kernel(BwdArgs a) {
 }
 
 // ============================================================================================
-// Delta = rowsum(dO * O) per (row, head), and LSE * log2(e) for the exp2-based kernels;
-// D/8 lanes per (row, head), 8 elements each.  A workgroup takes PRE_PASSES x (256 / (D/8))
-// consecutive rows of one head, so the per-head statistics ([head][row]) are written as
-// contiguous runs; every lane issues all its loads before the first product.
-// (row, head) pairs in memory order (O, dO and O_lo are [Ns][Hq][d]): D/8 lanes per pair, 8
-// elements each, so that every pass of a workgroup reads one contiguous span of each tensor
-constexpr int PRE_PASSES = 4;
+// Delta = rowsum(dO * O) per (row, head) (O + O_lo when the forward's residual is given),
+// LSE * log2(e) for the exp2-based kernels, and the (hi, lo) start values of the dK/dV kernel's
+// accumulators.  (row, head) pairs are walked in memory order (O, dO and O_lo are [Ns][Hq][d], the
+// statistics [Ns][Hq]): D/8 lanes per pair, 8 elements each, so that every pass of a workgroup
+// reads one contiguous span of each tensor and writes one run of each statistic; every lane issues
+// all its loads before the first product.  One pass per workgroup measured fastest (against two
+// and four: more workgroups in flight hide more of the load latency than more loads per lane).
+constexpr int PRE_PASSES = 1;
 template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   const int D = a.s.d, hq = a.s.hq, ns = a.s.ns;
